@@ -1,0 +1,60 @@
+"""Shape presets for one Llama-style decoder block (pre-norm, RMSNorm, RoPE,
+causal grouped-query attention, SwiGLU MLP), as named in the Litespark
+report's model description (Section 2.4, Table 1) and in the workloads this
+library is measured on.
+
+Pure data: no arithmetic of the method lives here.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, replace
+
+
+@dataclass(frozen=True)
+class BlockConfig:
+    name: str
+    cfg_id: int          # seeds the synthetic inputs (1000 * cfg_id + k)
+    batch: int
+    seq: int
+    hidden: int
+    n_q_heads: int
+    n_kv_heads: int
+    head_dim: int
+    intermediate: int
+    rope_theta: float
+    rms_eps: float = 1e-5
+
+    @property
+    def tokens(self) -> int:
+        return self.batch * self.seq
+
+    @property
+    def dq(self) -> int:
+        return self.n_q_heads * self.head_dim
+
+    @property
+    def dkv(self) -> int:
+        return self.n_kv_heads * self.head_dim
+
+    @property
+    def group(self) -> int:
+        return self.n_q_heads // self.n_kv_heads
+
+    def with_(self, **kw) -> "BlockConfig":
+        return replace(self, **kw)
+
+
+# Tiny block: parity case small enough for the fp64 oracle in well under a second.
+TINY = BlockConfig("tiny", 0, batch=2, seq=128, hidden=256, n_q_heads=4, n_kv_heads=2,
+                   head_dim=64, intermediate=688, rope_theta=1e4)
+# Llama-3.2-3B-shaped block at sequence 2048, batch 4: the measured workload.
+B3 = BlockConfig("3b", 1, batch=4, seq=2048, hidden=3072, n_q_heads=24, n_kv_heads=8,
+                 head_dim=128, intermediate=8192, rope_theta=5e5)
+# Same block at long context (attention-dominated).
+B3_8K = BlockConfig("3b_8k", 2, batch=1, seq=8192, hidden=3072, n_q_heads=24, n_kv_heads=8,
+                    head_dim=128, intermediate=8192, rope_theta=5e5)
+# Llama-30B-shaped block, multi-head attention (kv heads = q heads).
+B30 = BlockConfig("30b", 3, batch=2, seq=2048, hidden=6656, n_q_heads=52, n_kv_heads=52,
+                  head_dim=128, intermediate=17920, rope_theta=1e4)
+
+PRESETS = {c.name: c for c in (TINY, B3, B3_8K, B30)}

@@ -1,0 +1,41 @@
+"""FLOP accounting for the block and for whole-model throughput.
+
+Model FLOPs count each multiply-add as two FLOPs, the backward pass as twice
+the forward, and no recomputation.  Causal attention counts only the
+S(S+1)/2 query-key pairs that the mask keeps; the non-causal convention
+(the one the report's throughput tables follow, Tables 3 and 4) counts S^2.
+"""
+from __future__ import annotations
+
+from .configs import BlockConfig
+
+
+def block_params(hidden: int, dq: int, dkv: int, inter: int) -> int:
+    """Weights of the seven projections of one block (norm gains excluded)."""
+    return hidden * (dq + 2 * dkv) + dq * hidden + 3 * hidden * inter
+
+
+def block_fwd_flops(cfg: BlockConfig, causal: bool = True) -> float:
+    gemm = 2.0 * cfg.tokens * block_params(cfg.hidden, cfg.dq, cfg.dkv, cfg.intermediate)
+    pairs = cfg.seq * (cfg.seq + 1) / 2 if causal else float(cfg.seq) ** 2
+    attn = 4.0 * cfg.batch * cfg.n_q_heads * cfg.head_dim * pairs  # QK^T and PV
+    return gemm + attn
+
+
+def block_fwd_bwd_flops(cfg: BlockConfig, causal: bool = True) -> float:
+    """Model FLOPs of one forward plus backward pass (backward = 2 x forward)."""
+    return 3.0 * block_fwd_flops(cfg, causal)
+
+
+def attention_fwd_bwd_flops(cfg: BlockConfig, causal: bool = True) -> float:
+    pairs = cfg.seq * (cfg.seq + 1) / 2 if causal else float(cfg.seq) ** 2
+    return 3.0 * 4.0 * cfg.batch * cfg.n_q_heads * cfg.head_dim * pairs
+
+
+def training_flops_per_token(n_layers: int, hidden: int, n_heads: int, n_kv_heads: int,
+                             inter: int, vocab: int, seq: int) -> float:
+    """Whole-model training FLOPs per token, non-causal attention convention:
+    6 * (layer weights + LM head) + 12 * layers * hidden * seq."""
+    d = hidden // n_heads
+    n = n_layers * block_params(hidden, n_heads * d, n_kv_heads * d, inter) + vocab * hidden
+    return 6.0 * n + 12.0 * n_layers * hidden * seq
