@@ -1,0 +1,144 @@
+"""Benchmark: one Llama-style decoder block, forward + backward, on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--config 3b] [--no-cpu-baseline]
+
+A step is one ls_block_fwd_bwd call (RMSNorm, QKV + RoPE, causal GQA flash
+attention, output projection, RMSNorm, SwiGLU MLP, and the whole backward with
+all weight gradients accumulated in fp32) on the Llama-3.2-3B-shaped block at
+batch 4 x seq 2048 with seeded synthetic bf16 inputs already resident in HBM.
+Prints one JSON line (the last line of stdout).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "decoder-block fwd+bwd TFLOP/s and MFU (bf16), 3B shape seq 2048, 1 MI355X"
+PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 matrix peak (256 CUs x 4096 FLOP/clk x 2.4 GHz)
+PEAK_HBM_GBS = 8000.0
+DOMINANT = "gate/up projection"  # the largest single kernel launch of the step
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def dominant_flops(c) -> float:
+    """Algorithmic FLOPs of one gate/up projection launch: [T, H] x [H, 2I]."""
+    return 2.0 * c.tokens * (2 * c.intermediate) * c.hidden
+
+
+def cpu_baseline(c):
+    """The fp64 oracle on a bounded sample: one sequence of the workload."""
+    import numpy as np  # noqa: F401
+    from threadpoolctl import threadpool_info
+
+    from oracle import block as ob
+    from paper_2510_02483_amd import flops, inputs
+
+    one = c.with_(batch=1)
+    host = inputs.make_inputs(c)
+    f = inputs.to_f64({k: (v[:1] if k in ("x", "dy") else v) for k, v in host.items()})
+    w = {k: f[k] for k in ("wq", "wk", "wv", "wo", "wg", "wu", "wd", "attn_norm", "mlp_norm")}
+    t0 = time.perf_counter()
+    ob.block_fwd_bwd(f["x"], w, f["dy"], n_q_heads=c.n_q_heads, n_kv_heads=c.n_kv_heads,
+                     rope_theta=c.rope_theta, eps=c.rms_eps)
+    dt = time.perf_counter() - t0
+    threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
+    return {"value": flops.block_fwd_bwd_flops(one) / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"1 of {c.batch} sequences ({c.seq} tokens) of the same block, fp64 numpy oracle, "
+                      f"{dt:.1f} s wall"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="3b")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build runs the block on a single MI355X "
+              "(no sharding or collectives); run it with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2510_02483_amd import configs, flops, inputs, lib
+
+    c = configs.PRESETS[args.config]
+    log(f"config {c}")
+    host = inputs.make_inputs(c)
+    blk = lib.Block(c, host)
+    del host
+
+    for _ in range(args.warmup):
+        blk.step(accumulate=True)
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    lib.ls_timing_begin(DOMINANT, args.steps)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for _ in range(args.steps):
+        blk.step(accumulate=True)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    n_dom, dom_ms = lib.ls_timing_end()
+    ms = start.elapsed_time(stop) / args.steps
+
+    fl = flops.block_fwd_bwd_flops(c)
+    tflops = fl / (ms * 1e-3) / 1e12
+    dom_tflops = dominant_flops(c) / (dom_ms * 1e-3) / 1e12 if n_dom else None
+    result = {
+        "metric": METRIC,
+        "value": round(tflops, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"Llama-3.2-3B-shaped decoder block fwd+bwd, batch {c.batch} x seq {c.seq}",
+                   "batch": c.batch, "seq": c.seq, "hidden": c.hidden, "n_q_heads": c.n_q_heads,
+                   "n_kv_heads": c.n_kv_heads, "head_dim": c.head_dim, "intermediate": c.intermediate,
+                   "rope_theta": c.rope_theta, "parallelism": "single GPU"},
+        "mfu": round(tflops / PEAK_BF16_TFLOPS, 4),
+        "tokens_per_s": round(c.tokens / (ms * 1e-3), 1),
+        "model_flops_per_step": fl,
+        "tflops_noncausal_convention": round(flops.block_fwd_bwd_flops(c, causal=False) / (ms * 1e-3) / 1e12, 2),
+        "roofline": {
+            "kernel": f"{DOMINANT} (bf16 MFMA GEMM [T,H]x[H,2I] + fused SwiGLU)",
+            "bound": "mfma",
+            "achieved": round(dom_tflops, 2) if dom_tflops else None,
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(dom_tflops / PEAK_BF16_TFLOPS, 4) if dom_tflops else None,
+            "traffic": None,
+            "launches": n_dom,
+            "mean_ms": round(dom_ms, 4),
+        },
+    }
+    if not args.no_cpu_baseline and args.config == "3b":
+        log("timing the fp64 oracle on a one-sequence sample ...")
+        result["cpu_baseline"] = cpu_baseline(c)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,216 @@
+/*
+ * ls.h -- C ABI of the decoder-block library for AMD Instinct MI355X (gfx950).
+ *
+ * The library computes the forward and backward pass of one Llama-style
+ * decoder block, the part of a transformer whose attention and MLP layers the
+ * Litespark report (arXiv 2510.02483) speeds up (Section 1) while keeping the
+ * standard block's result (abstract, Section 5).  The block is the one the
+ * report's Section 2.4 describes: pre-norm RMSNorm, rotary position embedding,
+ * causal grouped-query attention (multi-head when kv heads = query heads) and
+ * a SwiGLU MLP, with residual adds:
+ *
+ *   x2 = x  + Wo . Attn(RoPE(Wq h1), RoPE(Wk h1), Wv h1),   h1 = RMSNorm(x;  g1)
+ *   y  = x2 + Wd . (silu(Wg h2) * (Wu h2)),                 h2 = RMSNorm(x2; g2)
+ *
+ * Conventions shared by every call
+ *   - Element types: activations, weights and upstream gradients are bf16
+ *     (raw bits in ls_bf16, round-to-nearest-even); all matrix products
+ *     accumulate in fp32; weight and RMSNorm-gain gradients are fp32
+ *     accumulators.
+ *   - Layouts: activations are row-major [batch * seq, features] (token-major);
+ *     projection weights are row-major [out_features, in_features]; RMSNorm
+ *     gains are [hidden].  q/k/v heads are contiguous blocks of head_dim
+ *     columns; query head h reads kv head h / (n_q_heads / n_kv_heads).
+ *   - RoPE: pairs (i, i + head_dim/2) of each head turn by p * theta^(-2i/d)
+ *     radians, p = 0..seq-1 restarting for every sequence.  Mask: causal,
+ *     key j <= query i.  Softmax scale 1/sqrt(head_dim).  LSE in natural log.
+ *   - Pointers: every pointer argument is device memory owned by the caller,
+ *     16-byte aligned, dense (no strides).  The library keeps no reference to
+ *     any of them after a call returns and allocates no device memory in any
+ *     call below; scratch space comes from the caller's workspace.
+ *   - Streams: `stream` is a hipStream_t (NULL = the null stream).  Calls only
+ *     enqueue work and return; device faults surface at the caller's next
+ *     synchronisation.  No host synchronisation happens inside a call.
+ *   - Errors: every call returns an ls_status.  Argument checks (null
+ *     pointers, shapes, alignment, aliasing, workspace size) all run before
+ *     any HIP call, so they behave identically on a host without a GPU.
+ *     ls_last_error() returns a thread-local description of the last failure.
+ *     No C++ exception crosses this interface.
+ *   - Gradient accumulation: `accumulate` = 0 overwrites the fp32 gradient
+ *     buffers, 1 adds into them.
+ *   - Calls that overlap on one stream are ordered; the library holds no
+ *     device state between calls, so calls on different streams with
+ *     disjoint buffers may run concurrently.
+ */
+#ifndef LS_H_
+#define LS_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef uint16_t ls_bf16;
+
+typedef enum {
+  LS_OK = 0,
+  LS_ERR_NULL = 1,        /* a required pointer is NULL */
+  LS_ERR_SHAPE = 2,       /* a size is non-positive, inconsistent or not a multiple of 8 */
+  LS_ERR_UNSUPPORTED = 3, /* valid but not implemented (head_dim not 64 or 128) */
+  LS_ERR_ALIGN = 4,       /* a pointer is not 16-byte aligned */
+  LS_ERR_ALIAS = 5,       /* an output buffer overlaps an input or another output */
+  LS_ERR_WORKSPACE = 6,   /* workspace or saved-state buffer too small */
+  LS_ERR_HIP = 7          /* the HIP runtime reported an error (see ls_last_error) */
+} ls_status;
+
+/* Shape of one decoder block.  Requirements: all sizes > 0; n_q_heads is a
+ * multiple of n_kv_heads; head_dim is 64 or 128; hidden and intermediate are
+ * multiples of 8; rms_eps >= 0, rope_theta > 1. */
+typedef struct {
+  int32_t batch;
+  int32_t seq;
+  int32_t hidden;
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t intermediate;
+  float rope_theta;
+  float rms_eps;
+} ls_block_cfg;
+
+/* bf16 weights, nn.Linear layout [out, in]:
+ *   wq [n_q_heads*head_dim, hidden], wk and wv [n_kv_heads*head_dim, hidden],
+ *   wo [hidden, n_q_heads*head_dim], wg and wu [intermediate, hidden],
+ *   wd [hidden, intermediate], attn_norm and mlp_norm [hidden]. */
+typedef struct {
+  const ls_bf16 *attn_norm, *wq, *wk, *wv, *wo, *mlp_norm, *wg, *wu, *wd;
+} ls_block_weights;
+
+/* fp32 gradient accumulators with the shapes of ls_block_weights. */
+typedef struct {
+  float *attn_norm, *wq, *wk, *wv, *wo, *mlp_norm, *wg, *wu, *wd;
+} ls_block_grads;
+
+/* Byte sizes for one configuration (each rounded up to 256 bytes). */
+typedef struct {
+  size_t attn_saved;     /* written by ls_attn_fwd, read by ls_attn_bwd */
+  size_t mlp_saved;      /* written by ls_mlp_fwd, read by ls_mlp_bwd */
+  size_t attn_workspace; /* scratch for ls_attn_fwd and ls_attn_bwd */
+  size_t mlp_workspace;  /* scratch for ls_mlp_fwd and ls_mlp_bwd */
+  size_t block_workspace;/* scratch for ls_block_fwd_bwd (includes both saved states) */
+} ls_sizes;
+
+/* Fill *out with the buffer sizes the calls below need for *cfg. */
+int ls_query_sizes(const ls_block_cfg* cfg, ls_sizes* out);
+
+/* Attention sub-layer forward (Section 2.4: RMSNorm, RoPE, causal GQA):
+ *   x2 = x + o Wo^T,  o = causal-softmax(q k^T / sqrt(d)) v,
+ *   q, k = RoPE(h1 Wq^T), RoPE(h1 Wk^T), v = h1 Wv^T, h1 = RMSNorm(x; attn_norm).
+ * x, x2: [batch*seq, hidden] bf16.  attn_saved: opaque, attn_saved bytes
+ * (holds h1, rotated q/k, v, o, the RMSNorm scales and the softmax log-sum-exp).
+ * x2 must not overlap x or attn_saved. */
+int ls_attn_fwd(const ls_block_cfg* cfg, const ls_bf16* x, const ls_block_weights* w,
+                ls_bf16* x2, void* attn_saved, void* workspace, size_t workspace_bytes,
+                void* stream);
+
+/* Attention sub-layer backward.  Given dx2 = dL/dx2, writes dx = dL/dx =
+ * dx2 + (d/dx of the attention branch)^T dx2 and the gradients of attn_norm,
+ * wq, wk, wv, wo (other members of *g are ignored and may be NULL).  The
+ * backward recomputes the softmax from the saved log-sum-exp.  x and
+ * attn_saved must be the ones ls_attn_fwd saw. */
+int ls_attn_bwd(const ls_block_cfg* cfg, const ls_bf16* x, const ls_block_weights* w,
+                const void* attn_saved, const ls_bf16* dx2, ls_bf16* dx,
+                const ls_block_grads* g, int accumulate, void* workspace,
+                size_t workspace_bytes, void* stream);
+
+/* MLP sub-layer forward (Section 2.4: RMSNorm, SwiGLU):
+ *   y = x2 + (silu(h2 Wg^T) * (h2 Wu^T)) Wd^T,  h2 = RMSNorm(x2; mlp_norm).
+ * mlp_saved: opaque, mlp_saved bytes (h2, gate and up outputs, their product,
+ * the RMSNorm scales). */
+int ls_mlp_fwd(const ls_block_cfg* cfg, const ls_bf16* x2, const ls_block_weights* w,
+               ls_bf16* y, void* mlp_saved, void* workspace, size_t workspace_bytes,
+               void* stream);
+
+/* MLP sub-layer backward: dx2 = dy + (d/dx2 of the MLP branch)^T dy and the
+ * gradients of mlp_norm, wg, wu, wd. */
+int ls_mlp_bwd(const ls_block_cfg* cfg, const ls_bf16* x2, const ls_block_weights* w,
+               const void* mlp_saved, const ls_bf16* dy, ls_bf16* dx2,
+               const ls_block_grads* g, int accumulate, void* workspace,
+               size_t workspace_bytes, void* stream);
+
+/* Whole block, forward then backward, in one call: writes y, dx and all nine
+ * weight gradients for upstream gradient dy.  workspace: block_workspace bytes. */
+int ls_block_fwd_bwd(const ls_block_cfg* cfg, const ls_bf16* x, const ls_block_weights* w,
+                     const ls_bf16* dy, ls_bf16* y, ls_bf16* dx, const ls_block_grads* g,
+                     int accumulate, void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---- single-kernel entry points (used for per-kernel parity) ---------------- */
+
+/* Causal attention core on a packed projection buffer.
+ * qkv: [batch*seq, (n_q_heads + 2*n_kv_heads)*head_dim] bf16, row = token,
+ * columns = q heads, then k heads, then v heads (q and k already rotated).
+ * o: [batch*seq, n_q_heads*head_dim] bf16.  lse: [batch, n_q_heads, seq] fp32.
+ * Only batch, seq, n_q_heads, n_kv_heads, head_dim of *cfg are used. */
+int ls_attn_core_fwd(const ls_block_cfg* cfg, const ls_bf16* qkv, ls_bf16* o, float* lse,
+                     void* stream);
+
+/* Backward of ls_attn_core_fwd: dqkv (same layout as qkv) from do, o, lse.
+ * The result holds gradients with respect to the rotated q and k (no inverse
+ * rotation).  workspace: at least ls_attn_core_bwd_workspace(cfg) bytes. */
+size_t ls_attn_core_bwd_workspace(const ls_block_cfg* cfg);
+int ls_attn_core_bwd(const ls_block_cfg* cfg, const ls_bf16* qkv, const ls_bf16* o,
+                     const float* lse, const ls_bf16* dout, ls_bf16* dqkv, void* workspace,
+                     size_t workspace_bytes, void* stream);
+
+/* RMSNorm over rows of length `hidden`: h = x * r * gamma, r = (mean x^2 + eps)^-1/2.
+ * x, h: [rows, hidden] bf16; r: [rows] fp32. */
+int ls_rmsnorm_fwd(int64_t rows, int32_t hidden, float eps, const ls_bf16* x,
+                   const ls_bf16* gamma, ls_bf16* h, float* r, void* stream);
+
+/* RMSNorm backward plus residual: dx = dres + r*(gamma*dh) - x*r^3*<gamma*dh, x>/hidden,
+ * dgamma (+)= sum over rows of dh * x * r.  dres may be NULL (treated as zero).
+ * workspace: at least ls_rmsnorm_bwd_workspace(rows, hidden) bytes. */
+size_t ls_rmsnorm_bwd_workspace(int64_t rows, int32_t hidden);
+int ls_rmsnorm_bwd(int64_t rows, int32_t hidden, const ls_bf16* x, const ls_bf16* gamma,
+                   const float* r, const ls_bf16* dh, const ls_bf16* dres, ls_bf16* dx,
+                   float* dgamma, int accumulate, void* workspace, size_t workspace_bytes,
+                   void* stream);
+
+/* Dense bf16 matrix products with fp32 accumulation (row-major operands):
+ *   ls_gemm_nt:  C[M,N]  = A[M,K] . B[N,K]^T          (forward projection)
+ *   ls_gemm_nn:  C[M,N]  = A[M,K] . B[K,N]            (input gradient)
+ *   ls_gemm_tn:  C[M,N] (+)= A[K,M]^T . B[K,N], fp32  (weight gradient)
+ * M, N, K > 0 and multiples of 8. */
+int ls_gemm_nt(int64_t M, int64_t N, int64_t K, const ls_bf16* A, const ls_bf16* B,
+               ls_bf16* C, void* stream);
+int ls_gemm_nn(int64_t M, int64_t N, int64_t K, const ls_bf16* A, const ls_bf16* B,
+               ls_bf16* C, void* stream);
+int ls_gemm_tn(int64_t M, int64_t N, int64_t K, const ls_bf16* A, const ls_bf16* B,
+               float* C, int accumulate, void* stream);
+
+/* ---- kernel timing (diagnostics) --------------------------------------------
+ * Measures one named kernel launch of the calls above with HIP events on the
+ * stream it runs on.  ls_timing_begin arms recording for launches whose label
+ * equals `label` (labels: "rmsnorm fwd", "qkv projection", "attention fwd",
+ * "output projection", "gate/up projection", "down projection", "dact",
+ * "dWd", "dh2", "dWg/dWu", "rmsnorm bwd", "dO", "dWo", "attention bwd",
+ * "dh1", "dWqkv"), creating up to max_launches event pairs up front;
+ * later calls record into them without allocating.  ls_timing_end waits for
+ * the recorded events, writes the number of recorded launches and their mean
+ * duration in milliseconds, disarms recording and releases the events.
+ * Process-wide; not meant for concurrent use from several threads. */
+int ls_timing_begin(const char* label, int max_launches);
+int ls_timing_end(int* launches, float* mean_ms);
+
+/* ---- diagnostics ------------------------------------------------------------ */
+const char* ls_status_string(int status);
+const char* ls_last_error(void);
+/* Library version as major*10000 + minor*100 + patch. */
+int ls_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LS_H_ */

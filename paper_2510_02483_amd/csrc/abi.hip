@@ -1,0 +1,874 @@
+// C ABI of the decoder-block library: argument validation (all of it before
+// any HIP call) and the orchestration of the kernels for each sub-layer.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <atomic>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+#include "ls.h"
+
+using ls::bf16_t;
+
+namespace {
+
+constexpr int kVersion = 100;  // 0.1.0
+
+thread_local std::string g_last_error;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* where) {
+  return fail(LS_ERR_HIP, "%s: %s (%d)", where, hipGetErrorString(e), (int)e);
+}
+
+#define LS_HIP(call, where)                          \
+  do {                                               \
+    hipError_t e_ = (call);                          \
+    if (e_ != hipSuccess) return hip_fail(e_, where); \
+  } while (0)
+
+inline size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// ---- optional per-launch timing (ls_timing_begin / ls_timing_end) -------------
+struct Timing {
+  std::mutex mu;
+  std::atomic<bool> armed{false};
+  std::string label;
+  std::vector<hipEvent_t> ev;  // start, stop per launch
+  int used = 0;
+};
+Timing g_timing;
+
+void timing_mark(const char* label, hipStream_t st, bool start) {
+  if (!g_timing.armed) return;
+  std::lock_guard<std::mutex> lk(g_timing.mu);
+  if (!g_timing.armed || g_timing.label != label) return;
+  const size_t idx = 2 * (size_t)g_timing.used + (start ? 0 : 1);
+  if (idx >= g_timing.ev.size()) return;
+  hipEventRecord(g_timing.ev[idx], st);
+  if (!start) ++g_timing.used;
+}
+
+// enqueue one labelled step, with timing marks around it
+#define LS_STEP(label, st, call)                         \
+  do {                                                  \
+    timing_mark(label, st, true);                       \
+    hipError_t e_ = (call);                             \
+    if (e_ != hipSuccess) return hip_fail(e_, label);   \
+    timing_mark(label, st, false);                      \
+  } while (0)
+
+struct Dims {
+  int64_t B, S, T, H, nq, nkv, d, Dq, Dkv, Dqkv, I;
+};
+
+Dims dims_of(const ls_block_cfg& c) {
+  Dims m;
+  m.B = c.batch;
+  m.S = c.seq;
+  m.T = (int64_t)c.batch * c.seq;
+  m.H = c.hidden;
+  m.nq = c.n_q_heads;
+  m.nkv = c.n_kv_heads;
+  m.d = c.head_dim;
+  m.Dq = m.nq * m.d;
+  m.Dkv = m.nkv * m.d;
+  m.Dqkv = m.Dq + 2 * m.Dkv;
+  m.I = c.intermediate;
+  return m;
+}
+
+int check_cfg(const ls_block_cfg* c) {
+  if (!c) return fail(LS_ERR_NULL, "cfg is NULL");
+  if (c->batch <= 0 || c->seq <= 0 || c->hidden <= 0 || c->n_q_heads <= 0 || c->n_kv_heads <= 0 ||
+      c->head_dim <= 0 || c->intermediate <= 0)
+    return fail(LS_ERR_SHAPE, "all sizes must be positive");
+  if (c->n_q_heads % c->n_kv_heads != 0)
+    return fail(LS_ERR_SHAPE, "n_q_heads (%d) is not a multiple of n_kv_heads (%d)", c->n_q_heads, c->n_kv_heads);
+  if (c->hidden % 8 != 0 || c->intermediate % 8 != 0)
+    return fail(LS_ERR_SHAPE, "hidden (%d) and intermediate (%d) must be multiples of 8", c->hidden, c->intermediate);
+  if (!(c->rope_theta > 1.0f) || !(c->rms_eps >= 0.0f))
+    return fail(LS_ERR_SHAPE, "rope_theta must exceed 1 and rms_eps must be >= 0");
+  if (c->head_dim != 64 && c->head_dim != 128)
+    return fail(LS_ERR_UNSUPPORTED, "head_dim %d is not supported (64 or 128)", c->head_dim);
+  if (c->hidden > 8192) return fail(LS_ERR_UNSUPPORTED, "hidden %d exceeds 8192", c->hidden);
+  const Dims m = dims_of(*c);
+  const int64_t lim = (int64_t)1 << 30;
+  if (m.T >= lim || m.Dqkv >= lim || 2 * m.I >= lim || m.T * std::max<int64_t>(m.Dqkv, 2 * m.I) >= ((int64_t)1 << 40))
+    return fail(LS_ERR_SHAPE, "problem too large");
+  return LS_OK;
+}
+
+bool misaligned(const void* p) { return ((uintptr_t)p & 15u) != 0; }
+
+struct Range {
+  const void* p;
+  size_t n;
+  const char* name;
+};
+
+bool overlaps(const Range& a, const Range& b) {
+  if (!a.p || !b.p || a.n == 0 || b.n == 0) return false;
+  const uintptr_t a0 = (uintptr_t)a.p, a1 = a0 + a.n, b0 = (uintptr_t)b.p, b1 = b0 + b.n;
+  return a0 < b1 && b0 < a1;
+}
+
+// every output range against every input range and every other output range
+int check_ranges(const std::vector<Range>& in, const std::vector<Range>& out) {
+  for (const Range& r : in) {
+    if (!r.p) return fail(LS_ERR_NULL, "%s is NULL", r.name);
+    if (misaligned(r.p)) return fail(LS_ERR_ALIGN, "%s is not 16-byte aligned", r.name);
+  }
+  for (const Range& r : out) {
+    if (!r.p) return fail(LS_ERR_NULL, "%s is NULL", r.name);
+    if (misaligned(r.p)) return fail(LS_ERR_ALIGN, "%s is not 16-byte aligned", r.name);
+  }
+  for (size_t i = 0; i < out.size(); ++i) {
+    for (const Range& r : in)
+      if (overlaps(out[i], r)) return fail(LS_ERR_ALIAS, "%s overlaps %s", out[i].name, r.name);
+    for (size_t j = i + 1; j < out.size(); ++j)
+      if (overlaps(out[i], out[j])) return fail(LS_ERR_ALIAS, "%s overlaps %s", out[i].name, out[j].name);
+  }
+  return LS_OK;
+}
+
+// ---- buffer layouts ------------------------------------------------------------
+
+struct Carver {
+  size_t off = 0;
+  size_t take(size_t bytes) {
+    const size_t o = off;
+    off += up256(bytes);
+    return o;
+  }
+};
+
+struct AttnSaved {
+  size_t h1, qkv, o, r1, lse, total;
+};
+AttnSaved attn_saved_layout(const Dims& m) {
+  Carver c;
+  AttnSaved s;
+  s.h1 = c.take(m.T * m.H * 2);
+  s.qkv = c.take(m.T * m.Dqkv * 2);
+  s.o = c.take(m.T * m.Dq * 2);
+  s.r1 = c.take(m.T * 4);
+  s.lse = c.take(m.B * m.nq * m.S * 4);
+  s.total = c.off;
+  return s;
+}
+
+struct MlpSaved {
+  size_t h2, gu, act, r2, total;
+};
+MlpSaved mlp_saved_layout(const Dims& m) {
+  Carver c;
+  MlpSaved s;
+  s.h2 = c.take(m.T * m.H * 2);
+  s.gu = c.take(m.T * 2 * m.I * 2);
+  s.act = c.take(m.T * m.I * 2);
+  s.r2 = c.take(m.T * 4);
+  s.total = c.off;
+  return s;
+}
+
+size_t norm_partial_bytes(const Dims& m) { return (size_t)ls::rmsnorm_bwd_parts(m.T) * m.H * 4; }
+
+ls::AttnShape attn_shape(const Dims& m) {
+  return ls::AttnShape{(int)m.B, (int)m.S, (int)m.nq, (int)m.nkv, (int)m.d};
+}
+
+struct AttnWs {
+  size_t rope, dO, dqkv, dh1, partial, core, total;
+};
+AttnWs attn_ws_layout(const Dims& m) {
+  Carver c;
+  AttnWs w;
+  w.rope = c.take(m.S * m.d * 4);  // cos and sin, S x d/2 each
+  w.dO = c.take(m.T * m.Dq * 2);
+  w.dqkv = c.take(m.T * m.Dqkv * 2);
+  w.dh1 = c.take(m.T * m.H * 2);
+  w.partial = c.take(norm_partial_bytes(m));
+  w.core = c.take(ls::attn_bwd_workspace(attn_shape(m)));
+  w.total = c.off;
+  return w;
+}
+
+struct MlpWs {
+  size_t dgu, dh2, partial, total;
+};
+MlpWs mlp_ws_layout(const Dims& m) {
+  Carver c;
+  MlpWs w;
+  w.dgu = c.take(m.T * 2 * m.I * 2);
+  w.dh2 = c.take(m.T * m.H * 2);
+  w.partial = c.take(norm_partial_bytes(m));
+  w.total = c.off;
+  return w;
+}
+
+struct BlockWs {
+  size_t attn_saved, mlp_saved, x2, dx2, scratch, total;
+};
+BlockWs block_ws_layout(const Dims& m) {
+  Carver c;
+  BlockWs w;
+  w.attn_saved = c.take(attn_saved_layout(m).total);
+  w.mlp_saved = c.take(mlp_saved_layout(m).total);
+  w.x2 = c.take(m.T * m.H * 2);
+  w.dx2 = c.take(m.T * m.H * 2);
+  w.scratch = c.take(std::max(attn_ws_layout(m).total, mlp_ws_layout(m).total));
+  w.total = c.off;
+  return w;
+}
+
+template <typename T>
+T* at(void* base, size_t off) {
+  return (T*)((char*)base + off);
+}
+template <typename T>
+const T* at(const void* base, size_t off) {
+  return (const T*)((const char*)base + off);
+}
+
+// ---- argument checks shared by the sub-layer calls --------------------------------
+
+void weight_ranges(const Dims& m, const ls_block_weights* w, bool attn, bool mlp, std::vector<Range>& v) {
+  if (attn) {
+    v.push_back({w->attn_norm, (size_t)m.H * 2, "w.attn_norm"});
+    v.push_back({w->wq, (size_t)(m.Dq * m.H * 2), "w.wq"});
+    v.push_back({w->wk, (size_t)(m.Dkv * m.H * 2), "w.wk"});
+    v.push_back({w->wv, (size_t)(m.Dkv * m.H * 2), "w.wv"});
+    v.push_back({w->wo, (size_t)(m.H * m.Dq * 2), "w.wo"});
+  }
+  if (mlp) {
+    v.push_back({w->mlp_norm, (size_t)m.H * 2, "w.mlp_norm"});
+    v.push_back({w->wg, (size_t)(m.I * m.H * 2), "w.wg"});
+    v.push_back({w->wu, (size_t)(m.I * m.H * 2), "w.wu"});
+    v.push_back({w->wd, (size_t)(m.H * m.I * 2), "w.wd"});
+  }
+}
+
+void grad_ranges(const Dims& m, const ls_block_grads* g, bool attn, bool mlp, std::vector<Range>& v) {
+  if (attn) {
+    v.push_back({g->attn_norm, (size_t)m.H * 4, "g.attn_norm"});
+    v.push_back({g->wq, (size_t)(m.Dq * m.H * 4), "g.wq"});
+    v.push_back({g->wk, (size_t)(m.Dkv * m.H * 4), "g.wk"});
+    v.push_back({g->wv, (size_t)(m.Dkv * m.H * 4), "g.wv"});
+    v.push_back({g->wo, (size_t)(m.H * m.Dq * 4), "g.wo"});
+  }
+  if (mlp) {
+    v.push_back({g->mlp_norm, (size_t)m.H * 4, "g.mlp_norm"});
+    v.push_back({g->wg, (size_t)(m.I * m.H * 4), "g.wg"});
+    v.push_back({g->wu, (size_t)(m.I * m.H * 4), "g.wu"});
+    v.push_back({g->wd, (size_t)(m.H * m.I * 4), "g.wd"});
+  }
+}
+
+// ---- the sub-layers (arguments already checked) ------------------------------------
+
+int run_attn_fwd(const ls_block_cfg& cfg, const Dims& m, const bf16_t* x, const ls_block_weights* w, bf16_t* x2,
+                 void* saved, void* ws, hipStream_t st) {
+  const AttnSaved sv = attn_saved_layout(m);
+  const AttnWs wl = attn_ws_layout(m);
+  bf16_t* h1 = at<bf16_t>(saved, sv.h1);
+  bf16_t* qkv = at<bf16_t>(saved, sv.qkv);
+  bf16_t* o = at<bf16_t>(saved, sv.o);
+  float* r1 = at<float>(saved, sv.r1);
+  float* lse = at<float>(saved, sv.lse);
+  float* cs = at<float>(ws, wl.rope);
+  LS_STEP("rmsnorm fwd", st, ls::rmsnorm_fwd(m.T, (int)m.H, cfg.rms_eps, x, (const bf16_t*)w->attn_norm, h1, r1, st));
+  LS_STEP("rope table", st, ls::rope_table((int)m.S, (int)m.d, (double)cfg.rope_theta, cs, st));
+  ls::GemmArgs g;
+  g.M = (int)m.T;
+  g.N = (int)m.Dqkv;
+  g.K = (int)m.H;
+  g.A = h1;
+  g.lda = m.H;
+  g.B[0] = (const bf16_t*)w->wq;
+  g.B[1] = (const bf16_t*)w->wk;
+  g.B[2] = (const bf16_t*)w->wv;
+  g.b_start[1] = (int)m.Dq;
+  g.b_start[2] = (int)(m.Dq + m.Dkv);
+  g.ldb = m.H;
+  g.epi = ls::EPI_ROPE;
+  g.C = qkv;
+  g.ldc = m.Dqkv;
+  g.rope_cs = cs;
+  g.seq = (int)m.S;
+  g.head_dim = (int)m.d;
+  g.rope_cols = (int)(m.Dq + m.Dkv);
+  LS_STEP("qkv projection", st, ls::gemm(g, st));
+  LS_STEP("attention fwd", st, ls::attn_fwd(attn_shape(m), qkv, o, lse, st));
+  ls::GemmArgs p;
+  p.M = (int)m.T;
+  p.N = (int)m.H;
+  p.K = (int)m.Dq;
+  p.A = o;
+  p.lda = m.Dq;
+  p.B[0] = (const bf16_t*)w->wo;
+  p.ldb = m.Dq;
+  p.epi = ls::EPI_RESID;
+  p.R = x;
+  p.C = x2;
+  p.ldc = m.H;
+  LS_STEP("output projection", st, ls::gemm(p, st));
+  return LS_OK;
+}
+
+int run_attn_bwd(const ls_block_cfg& cfg, const Dims& m, const bf16_t* x, const ls_block_weights* w,
+                 const void* saved, const bf16_t* dx2, bf16_t* dx, const ls_block_grads* gr, int accumulate, void* ws,
+                 hipStream_t st) {
+  const AttnSaved sv = attn_saved_layout(m);
+  const AttnWs wl = attn_ws_layout(m);
+  const bf16_t* h1 = at<bf16_t>(saved, sv.h1);
+  const bf16_t* qkv = at<bf16_t>(saved, sv.qkv);
+  const bf16_t* o = at<bf16_t>(saved, sv.o);
+  const float* r1 = at<float>(saved, sv.r1);
+  const float* lse = at<float>(saved, sv.lse);
+  float* cs = at<float>(ws, wl.rope);
+  bf16_t* dO = at<bf16_t>(ws, wl.dO);
+  bf16_t* dqkv = at<bf16_t>(ws, wl.dqkv);
+  bf16_t* dh1 = at<bf16_t>(ws, wl.dh1);
+  float* partial = at<float>(ws, wl.partial);
+  void* core = at<char>(ws, wl.core);
+  LS_STEP("rope table", st, ls::rope_table((int)m.S, (int)m.d, (double)cfg.rope_theta, cs, st));
+  {  // dO = dx2 Wo
+    ls::GemmArgs g;
+    g.M = (int)m.T;
+    g.N = (int)m.Dq;
+    g.K = (int)m.H;
+    g.A = dx2;
+    g.lda = m.H;
+    g.B[0] = (const bf16_t*)w->wo;
+    g.ldb = m.Dq;
+    g.b_kcontig = false;
+    g.epi = ls::EPI_BF16;
+    g.C = dO;
+    g.ldc = m.Dq;
+    LS_STEP("dO", st, ls::gemm(g, st));
+  }
+  {  // dWo (+)= dx2^T o
+    ls::GemmArgs g;
+    g.M = (int)m.H;
+    g.N = (int)m.Dq;
+    g.K = (int)m.T;
+    g.A = dx2;
+    g.lda = m.H;
+    g.a_kcontig = false;
+    g.B[0] = o;
+    g.ldb = m.Dq;
+    g.b_kcontig = false;
+    g.epi = ls::EPI_F32;
+    g.F[0] = gr->wo;
+    g.ldf = m.Dq;
+    g.accumulate = accumulate;
+    LS_STEP("dWo", st, ls::gemm(g, st));
+  }
+  LS_STEP("attention bwd", st, ls::attn_bwd(attn_shape(m), qkv, o, lse, dO, dqkv, cs, core, st));
+  {  // dh1 = dq Wq + dk Wk + dv Wv
+    ls::GemmArgs g;
+    g.M = (int)m.T;
+    g.N = (int)m.H;
+    g.K = (int)m.Dqkv;
+    g.A = dqkv;
+    g.lda = m.Dqkv;
+    g.B[0] = (const bf16_t*)w->wq;
+    g.B[1] = (const bf16_t*)w->wk;
+    g.B[2] = (const bf16_t*)w->wv;
+    g.b_start[1] = (int)m.Dq;
+    g.b_start[2] = (int)(m.Dq + m.Dkv);
+    g.ldb = m.H;
+    g.b_kcontig = false;
+    g.epi = ls::EPI_BF16;
+    g.C = dh1;
+    g.ldc = m.H;
+    LS_STEP("dh1", st, ls::gemm(g, st));
+  }
+  {  // dWq, dWk, dWv (+)= dqkv^T h1
+    ls::GemmArgs g;
+    g.M = (int)m.Dqkv;
+    g.N = (int)m.H;
+    g.K = (int)m.T;
+    g.A = dqkv;
+    g.lda = m.Dqkv;
+    g.a_kcontig = false;
+    g.B[0] = h1;
+    g.ldb = m.H;
+    g.b_kcontig = false;
+    g.epi = ls::EPI_F32;
+    g.F[0] = gr->wq;
+    g.F[1] = gr->wk;
+    g.F[2] = gr->wv;
+    g.f_start[1] = (int)m.Dq;
+    g.f_start[2] = (int)(m.Dq + m.Dkv);
+    g.ldf = m.H;
+    g.accumulate = accumulate;
+    LS_STEP("dWqkv", st, ls::gemm(g, st));
+  }
+  LS_STEP("rmsnorm bwd", st,
+          ls::rmsnorm_bwd(m.T, (int)m.H, x, (const bf16_t*)w->attn_norm, r1, dh1, dx2, dx, gr->attn_norm, accumulate,
+                          partial, st));
+  return LS_OK;
+}
+
+int run_mlp_fwd(const ls_block_cfg& cfg, const Dims& m, const bf16_t* x2, const ls_block_weights* w, bf16_t* y,
+                void* saved, hipStream_t st) {
+  const MlpSaved sv = mlp_saved_layout(m);
+  bf16_t* h2 = at<bf16_t>(saved, sv.h2);
+  bf16_t* gu = at<bf16_t>(saved, sv.gu);
+  bf16_t* act = at<bf16_t>(saved, sv.act);
+  float* r2 = at<float>(saved, sv.r2);
+  LS_STEP("rmsnorm fwd", st, ls::rmsnorm_fwd(m.T, (int)m.H, cfg.rms_eps, x2, (const bf16_t*)w->mlp_norm, h2, r2, st));
+  {
+    ls::GemmArgs g;
+    g.M = (int)m.T;
+    g.N = (int)(2 * ((m.I + 63) / 64) * 64);
+    g.K = (int)m.H;
+    g.A = h2;
+    g.lda = m.H;
+    g.B[0] = (const bf16_t*)w->wg;
+    g.B[1] = (const bf16_t*)w->wu;
+    g.glu = true;
+    g.glu_rows = (int)m.I;
+    g.ldb = m.H;
+    g.epi = ls::EPI_GLU_FWD;
+    g.C = gu;
+    g.ldc = 2 * m.I;
+    g.act = act;
+    g.glu_I = (int)m.I;
+    LS_STEP("gate/up projection", st, ls::gemm(g, st));
+  }
+  {
+    ls::GemmArgs g;
+    g.M = (int)m.T;
+    g.N = (int)m.H;
+    g.K = (int)m.I;
+    g.A = act;
+    g.lda = m.I;
+    g.B[0] = (const bf16_t*)w->wd;
+    g.ldb = m.I;
+    g.epi = ls::EPI_RESID;
+    g.R = x2;
+    g.C = y;
+    g.ldc = m.H;
+    LS_STEP("down projection", st, ls::gemm(g, st));
+  }
+  return LS_OK;
+}
+
+int run_mlp_bwd(const ls_block_cfg& cfg, const Dims& m, const bf16_t* x2, const ls_block_weights* w,
+                const void* saved, const bf16_t* dy, bf16_t* dx2, const ls_block_grads* gr, int accumulate, void* ws,
+                hipStream_t st) {
+  (void)cfg;
+  const MlpSaved sv = mlp_saved_layout(m);
+  const MlpWs wl = mlp_ws_layout(m);
+  const bf16_t* h2 = at<bf16_t>(saved, sv.h2);
+  const bf16_t* gu = at<bf16_t>(saved, sv.gu);
+  const bf16_t* act = at<bf16_t>(saved, sv.act);
+  const float* r2 = at<float>(saved, sv.r2);
+  bf16_t* dgu = at<bf16_t>(ws, wl.dgu);
+  bf16_t* dh2 = at<bf16_t>(ws, wl.dh2);
+  float* partial = at<float>(ws, wl.partial);
+  {  // dact = dy Wd, then dg, du from the saved gate/up outputs
+    ls::GemmArgs g;
+    g.M = (int)m.T;
+    g.N = (int)m.I;
+    g.K = (int)m.H;
+    g.A = dy;
+    g.lda = m.H;
+    g.B[0] = (const bf16_t*)w->wd;
+    g.ldb = m.I;
+    g.b_kcontig = false;
+    g.epi = ls::EPI_GLU_BWD;
+    g.C = dgu;
+    g.ldc = 2 * m.I;
+    g.gu_in = gu;
+    g.glu_I = (int)m.I;
+    LS_STEP("dact", st, ls::gemm(g, st));
+  }
+  {  // dWd (+)= dy^T act
+    ls::GemmArgs g;
+    g.M = (int)m.H;
+    g.N = (int)m.I;
+    g.K = (int)m.T;
+    g.A = dy;
+    g.lda = m.H;
+    g.a_kcontig = false;
+    g.B[0] = act;
+    g.ldb = m.I;
+    g.b_kcontig = false;
+    g.epi = ls::EPI_F32;
+    g.F[0] = gr->wd;
+    g.ldf = m.I;
+    g.accumulate = accumulate;
+    LS_STEP("dWd", st, ls::gemm(g, st));
+  }
+  {  // dh2 = dg Wg + du Wu
+    ls::GemmArgs g;
+    g.M = (int)m.T;
+    g.N = (int)m.H;
+    g.K = (int)(2 * m.I);
+    g.A = dgu;
+    g.lda = 2 * m.I;
+    g.B[0] = (const bf16_t*)w->wg;
+    g.B[1] = (const bf16_t*)w->wu;
+    g.b_start[1] = (int)m.I;
+    g.ldb = m.H;
+    g.b_kcontig = false;
+    g.epi = ls::EPI_BF16;
+    g.C = dh2;
+    g.ldc = m.H;
+    LS_STEP("dh2", st, ls::gemm(g, st));
+  }
+  {  // dWg, dWu (+)= [dg du]^T h2
+    ls::GemmArgs g;
+    g.M = (int)(2 * m.I);
+    g.N = (int)m.H;
+    g.K = (int)m.T;
+    g.A = dgu;
+    g.lda = 2 * m.I;
+    g.a_kcontig = false;
+    g.B[0] = h2;
+    g.ldb = m.H;
+    g.b_kcontig = false;
+    g.epi = ls::EPI_F32;
+    g.F[0] = gr->wg;
+    g.F[1] = gr->wu;
+    g.f_start[1] = (int)m.I;
+    g.ldf = m.H;
+    g.accumulate = accumulate;
+    LS_STEP("dWg/dWu", st, ls::gemm(g, st));
+  }
+  LS_STEP("rmsnorm bwd", st,
+          ls::rmsnorm_bwd(m.T, (int)m.H, x2, (const bf16_t*)w->mlp_norm, r2, dh2, dy, dx2, gr->mlp_norm, accumulate,
+                          partial, st));
+  return LS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int ls_version(void) { return kVersion; }
+
+const char* ls_last_error(void) { return g_last_error.c_str(); }
+
+const char* ls_status_string(int status) {
+  switch (status) {
+    case LS_OK: return "ok";
+    case LS_ERR_NULL: return "null pointer";
+    case LS_ERR_SHAPE: return "invalid shape";
+    case LS_ERR_UNSUPPORTED: return "unsupported configuration";
+    case LS_ERR_ALIGN: return "misaligned pointer";
+    case LS_ERR_ALIAS: return "overlapping buffers";
+    case LS_ERR_WORKSPACE: return "workspace too small";
+    case LS_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+int ls_query_sizes(const ls_block_cfg* cfg, ls_sizes* out) {
+  if (int e = check_cfg(cfg)) return e;
+  if (!out) return fail(LS_ERR_NULL, "out is NULL");
+  const Dims m = dims_of(*cfg);
+  out->attn_saved = attn_saved_layout(m).total;
+  out->mlp_saved = mlp_saved_layout(m).total;
+  out->attn_workspace = attn_ws_layout(m).total;
+  out->mlp_workspace = mlp_ws_layout(m).total;
+  out->block_workspace = block_ws_layout(m).total;
+  return LS_OK;
+}
+
+int ls_attn_fwd(const ls_block_cfg* cfg, const ls_bf16* x, const ls_block_weights* w, ls_bf16* x2, void* attn_saved,
+                void* workspace, size_t workspace_bytes, void* stream) {
+  if (int e = check_cfg(cfg)) return e;
+  if (!w) return fail(LS_ERR_NULL, "weights is NULL");
+  const Dims m = dims_of(*cfg);
+  const size_t act = (size_t)(m.T * m.H * 2);
+  std::vector<Range> in{{x, act, "x"}}, out{{x2, act, "x2"},
+                                           {attn_saved, attn_saved_layout(m).total, "attn_saved"},
+                                           {workspace, workspace_bytes, "workspace"}};
+  weight_ranges(m, w, true, false, in);
+  if (int e = check_ranges(in, out)) return e;
+  if (workspace_bytes < attn_ws_layout(m).total)
+    return fail(LS_ERR_WORKSPACE, "workspace %zu < %zu bytes", workspace_bytes, attn_ws_layout(m).total);
+  return run_attn_fwd(*cfg, m, (const bf16_t*)x, w, (bf16_t*)x2, attn_saved, workspace, (hipStream_t)stream);
+}
+
+int ls_attn_bwd(const ls_block_cfg* cfg, const ls_bf16* x, const ls_block_weights* w, const void* attn_saved,
+                const ls_bf16* dx2, ls_bf16* dx, const ls_block_grads* g, int accumulate, void* workspace,
+                size_t workspace_bytes, void* stream) {
+  if (int e = check_cfg(cfg)) return e;
+  if (!w || !g) return fail(LS_ERR_NULL, "weights or grads is NULL");
+  const Dims m = dims_of(*cfg);
+  const size_t act = (size_t)(m.T * m.H * 2);
+  std::vector<Range> in{{x, act, "x"}, {attn_saved, attn_saved_layout(m).total, "attn_saved"}, {dx2, act, "dx2"}};
+  std::vector<Range> out{{dx, act, "dx"}, {workspace, workspace_bytes, "workspace"}};
+  weight_ranges(m, w, true, false, in);
+  grad_ranges(m, g, true, false, out);
+  if (int e = check_ranges(in, out)) return e;
+  if (workspace_bytes < attn_ws_layout(m).total)
+    return fail(LS_ERR_WORKSPACE, "workspace %zu < %zu bytes", workspace_bytes, attn_ws_layout(m).total);
+  return run_attn_bwd(*cfg, m, (const bf16_t*)x, w, attn_saved, (const bf16_t*)dx2, (bf16_t*)dx, g, accumulate != 0,
+                      workspace, (hipStream_t)stream);
+}
+
+int ls_mlp_fwd(const ls_block_cfg* cfg, const ls_bf16* x2, const ls_block_weights* w, ls_bf16* y, void* mlp_saved,
+               void* workspace, size_t workspace_bytes, void* stream) {
+  if (int e = check_cfg(cfg)) return e;
+  if (!w) return fail(LS_ERR_NULL, "weights is NULL");
+  const Dims m = dims_of(*cfg);
+  const size_t act = (size_t)(m.T * m.H * 2);
+  std::vector<Range> in{{x2, act, "x2"}}, out{{y, act, "y"}, {mlp_saved, mlp_saved_layout(m).total, "mlp_saved"}};
+  if (workspace) out.push_back({workspace, workspace_bytes, "workspace"});
+  weight_ranges(m, w, false, true, in);
+  if (int e = check_ranges(in, out)) return e;
+  return run_mlp_fwd(*cfg, m, (const bf16_t*)x2, w, (bf16_t*)y, mlp_saved, (hipStream_t)stream);
+}
+
+int ls_mlp_bwd(const ls_block_cfg* cfg, const ls_bf16* x2, const ls_block_weights* w, const void* mlp_saved,
+               const ls_bf16* dy, ls_bf16* dx2, const ls_block_grads* g, int accumulate, void* workspace,
+               size_t workspace_bytes, void* stream) {
+  if (int e = check_cfg(cfg)) return e;
+  if (!w || !g) return fail(LS_ERR_NULL, "weights or grads is NULL");
+  const Dims m = dims_of(*cfg);
+  const size_t act = (size_t)(m.T * m.H * 2);
+  std::vector<Range> in{{x2, act, "x2"}, {mlp_saved, mlp_saved_layout(m).total, "mlp_saved"}, {dy, act, "dy"}};
+  std::vector<Range> out{{dx2, act, "dx2"}, {workspace, workspace_bytes, "workspace"}};
+  weight_ranges(m, w, false, true, in);
+  grad_ranges(m, g, false, true, out);
+  if (int e = check_ranges(in, out)) return e;
+  if (workspace_bytes < mlp_ws_layout(m).total)
+    return fail(LS_ERR_WORKSPACE, "workspace %zu < %zu bytes", workspace_bytes, mlp_ws_layout(m).total);
+  return run_mlp_bwd(*cfg, m, (const bf16_t*)x2, w, mlp_saved, (const bf16_t*)dy, (bf16_t*)dx2, g, accumulate != 0,
+                     workspace, (hipStream_t)stream);
+}
+
+int ls_block_fwd_bwd(const ls_block_cfg* cfg, const ls_bf16* x, const ls_block_weights* w, const ls_bf16* dy,
+                     ls_bf16* y, ls_bf16* dx, const ls_block_grads* g, int accumulate, void* workspace,
+                     size_t workspace_bytes, void* stream) {
+  if (int e = check_cfg(cfg)) return e;
+  if (!w || !g) return fail(LS_ERR_NULL, "weights or grads is NULL");
+  const Dims m = dims_of(*cfg);
+  const size_t act = (size_t)(m.T * m.H * 2);
+  const BlockWs bl = block_ws_layout(m);
+  std::vector<Range> in{{x, act, "x"}, {dy, act, "dy"}};
+  std::vector<Range> out{{y, act, "y"}, {dx, act, "dx"}, {workspace, workspace_bytes, "workspace"}};
+  weight_ranges(m, w, true, true, in);
+  grad_ranges(m, g, true, true, out);
+  if (int e = check_ranges(in, out)) return e;
+  if (workspace_bytes < bl.total)
+    return fail(LS_ERR_WORKSPACE, "workspace %zu < %zu bytes", workspace_bytes, bl.total);
+  const hipStream_t st = (hipStream_t)stream;
+  void* asv = at<char>(workspace, bl.attn_saved);
+  void* msv = at<char>(workspace, bl.mlp_saved);
+  bf16_t* x2 = at<bf16_t>(workspace, bl.x2);
+  bf16_t* dx2 = at<bf16_t>(workspace, bl.dx2);
+  void* scratch = at<char>(workspace, bl.scratch);
+  const int acc = accumulate != 0;
+  if (int e = run_attn_fwd(*cfg, m, (const bf16_t*)x, w, x2, asv, scratch, st)) return e;
+  if (int e = run_mlp_fwd(*cfg, m, x2, w, (bf16_t*)y, msv, st)) return e;
+  if (int e = run_mlp_bwd(*cfg, m, x2, w, msv, (const bf16_t*)dy, dx2, g, acc, scratch, st)) return e;
+  return run_attn_bwd(*cfg, m, (const bf16_t*)x, w, asv, dx2, (bf16_t*)dx, g, acc, scratch, st);
+}
+
+int ls_timing_begin(const char* label, int max_launches) {
+  if (!label) return fail(LS_ERR_NULL, "label is NULL");
+  if (max_launches <= 0 || max_launches > 100000) return fail(LS_ERR_SHAPE, "max_launches out of range");
+  std::lock_guard<std::mutex> lk(g_timing.mu);
+  for (hipEvent_t e : g_timing.ev) hipEventDestroy(e);
+  g_timing.ev.clear();
+  g_timing.armed = false;
+  for (int i = 0; i < 2 * max_launches; ++i) {
+    hipEvent_t e;
+    hipError_t r = hipEventCreate(&e);
+    if (r != hipSuccess) {
+      for (hipEvent_t x : g_timing.ev) hipEventDestroy(x);
+      g_timing.ev.clear();
+      return hip_fail(r, "hipEventCreate");
+    }
+    g_timing.ev.push_back(e);
+  }
+  g_timing.label = label;
+  g_timing.used = 0;
+  g_timing.armed = true;
+  return LS_OK;
+}
+
+int ls_timing_end(int* launches, float* mean_ms) {
+  if (!launches || !mean_ms) return fail(LS_ERR_NULL, "output pointer is NULL");
+  std::lock_guard<std::mutex> lk(g_timing.mu);
+  g_timing.armed = false;
+  double total = 0.0;
+  int n = g_timing.used;
+  int rc = LS_OK;
+  for (int i = 0; i < n && rc == LS_OK; ++i) {
+    float ms = 0.f;
+    hipError_t r = hipEventSynchronize(g_timing.ev[2 * i + 1]);
+    if (r == hipSuccess) r = hipEventElapsedTime(&ms, g_timing.ev[2 * i], g_timing.ev[2 * i + 1]);
+    if (r != hipSuccess) rc = hip_fail(r, "timing events");
+    total += ms;
+  }
+  for (hipEvent_t e : g_timing.ev) hipEventDestroy(e);
+  g_timing.ev.clear();
+  g_timing.used = 0;
+  *launches = n;
+  *mean_ms = n ? (float)(total / n) : 0.f;
+  return rc;
+}
+
+// ---- single-kernel entry points ------------------------------------------------------
+
+int ls_attn_core_fwd(const ls_block_cfg* cfg, const ls_bf16* qkv, ls_bf16* o, float* lse, void* stream) {
+  if (int e = check_cfg(cfg)) return e;
+  const Dims m = dims_of(*cfg);
+  std::vector<Range> in{{qkv, (size_t)(m.T * m.Dqkv * 2), "qkv"}};
+  std::vector<Range> out{{o, (size_t)(m.T * m.Dq * 2), "o"}, {lse, (size_t)(m.B * m.nq * m.S * 4), "lse"}};
+  if (int e = check_ranges(in, out)) return e;
+  LS_HIP(ls::attn_fwd(attn_shape(m), (const bf16_t*)qkv, (bf16_t*)o, lse, (hipStream_t)stream), "attention forward");
+  return LS_OK;
+}
+
+size_t ls_attn_core_bwd_workspace(const ls_block_cfg* cfg) {
+  if (check_cfg(cfg)) return 0;
+  return ls::attn_bwd_workspace(attn_shape(dims_of(*cfg)));
+}
+
+int ls_attn_core_bwd(const ls_block_cfg* cfg, const ls_bf16* qkv, const ls_bf16* o, const float* lse,
+                     const ls_bf16* dout, ls_bf16* dqkv, void* workspace, size_t workspace_bytes, void* stream) {
+  if (int e = check_cfg(cfg)) return e;
+  const Dims m = dims_of(*cfg);
+  const size_t need = ls::attn_bwd_workspace(attn_shape(m));
+  std::vector<Range> in{{qkv, (size_t)(m.T * m.Dqkv * 2), "qkv"},
+                        {o, (size_t)(m.T * m.Dq * 2), "o"},
+                        {lse, (size_t)(m.B * m.nq * m.S * 4), "lse"},
+                        {dout, (size_t)(m.T * m.Dq * 2), "dout"}};
+  std::vector<Range> out{{dqkv, (size_t)(m.T * m.Dqkv * 2), "dqkv"}, {workspace, workspace_bytes, "workspace"}};
+  if (int e = check_ranges(in, out)) return e;
+  if (workspace_bytes < need) return fail(LS_ERR_WORKSPACE, "workspace %zu < %zu bytes", workspace_bytes, need);
+  LS_HIP(ls::attn_bwd(attn_shape(m), (const bf16_t*)qkv, (const bf16_t*)o, lse, (const bf16_t*)dout, (bf16_t*)dqkv,
+                      nullptr, workspace, (hipStream_t)stream),
+         "attention backward");
+  return LS_OK;
+}
+
+static int check_norm_shape(int64_t rows, int32_t hidden) {
+  if (rows <= 0 || hidden <= 0) return fail(LS_ERR_SHAPE, "rows and hidden must be positive");
+  if (hidden % 8) return fail(LS_ERR_SHAPE, "hidden %d is not a multiple of 8", hidden);
+  if (hidden > 8192) return fail(LS_ERR_UNSUPPORTED, "hidden %d exceeds 8192", hidden);
+  if (rows >= ((int64_t)1 << 31)) return fail(LS_ERR_SHAPE, "too many rows");
+  return LS_OK;
+}
+
+int ls_rmsnorm_fwd(int64_t rows, int32_t hidden, float eps, const ls_bf16* x, const ls_bf16* gamma, ls_bf16* h,
+                   float* r, void* stream) {
+  if (int e = check_norm_shape(rows, hidden)) return e;
+  if (!(eps >= 0.0f)) return fail(LS_ERR_SHAPE, "eps must be >= 0");
+  const size_t act = (size_t)rows * hidden * 2;
+  std::vector<Range> in{{x, act, "x"}, {gamma, (size_t)hidden * 2, "gamma"}};
+  std::vector<Range> out{{h, act, "h"}, {r, (size_t)rows * 4, "r"}};
+  if (int e = check_ranges(in, out)) return e;
+  LS_HIP(ls::rmsnorm_fwd(rows, hidden, eps, (const bf16_t*)x, (const bf16_t*)gamma, (bf16_t*)h, r, (hipStream_t)stream),
+         "rmsnorm_fwd");
+  return LS_OK;
+}
+
+size_t ls_rmsnorm_bwd_workspace(int64_t rows, int32_t hidden) {
+  if (rows <= 0 || hidden <= 0) return 0;
+  return (size_t)ls::rmsnorm_bwd_parts(rows) * hidden * 4;
+}
+
+int ls_rmsnorm_bwd(int64_t rows, int32_t hidden, const ls_bf16* x, const ls_bf16* gamma, const float* r,
+                   const ls_bf16* dh, const ls_bf16* dres, ls_bf16* dx, float* dgamma, int accumulate, void* workspace,
+                   size_t workspace_bytes, void* stream) {
+  if (int e = check_norm_shape(rows, hidden)) return e;
+  const size_t act = (size_t)rows * hidden * 2;
+  std::vector<Range> in{{x, act, "x"}, {gamma, (size_t)hidden * 2, "gamma"}, {r, (size_t)rows * 4, "r"}, {dh, act, "dh"}};
+  if (dres) in.push_back({dres, act, "dres"});
+  std::vector<Range> out{{dx, act, "dx"}, {dgamma, (size_t)hidden * 4, "dgamma"}, {workspace, workspace_bytes, "workspace"}};
+  if (int e = check_ranges(in, out)) return e;
+  const size_t need = ls_rmsnorm_bwd_workspace(rows, hidden);
+  if (workspace_bytes < need) return fail(LS_ERR_WORKSPACE, "workspace %zu < %zu bytes", workspace_bytes, need);
+  LS_HIP(ls::rmsnorm_bwd(rows, hidden, (const bf16_t*)x, (const bf16_t*)gamma, r, (const bf16_t*)dh,
+                         (const bf16_t*)dres, (bf16_t*)dx, dgamma, accumulate != 0, (float*)workspace,
+                         (hipStream_t)stream),
+         "rmsnorm_bwd");
+  return LS_OK;
+}
+
+static int check_gemm(int64_t M, int64_t N, int64_t K) {
+  if (M <= 0 || N <= 0 || K <= 0) return fail(LS_ERR_SHAPE, "M, N, K must be positive");
+  if (M % 8 || N % 8 || K % 8) return fail(LS_ERR_SHAPE, "M, N, K must be multiples of 8");
+  if (M >= (1 << 30) || N >= (1 << 30) || K >= (1 << 30)) return fail(LS_ERR_SHAPE, "dimension too large");
+  return LS_OK;
+}
+
+static int gemm_common(int64_t M, int64_t N, int64_t K, const void* A, const void* B, void* C, size_t c_elem,
+                       ls::GemmArgs& g) {
+  if (int e = check_gemm(M, N, K)) return e;
+  std::vector<Range> in{{A, (size_t)(M * K * 2), "A"}, {B, (size_t)(K * N * 2), "B"}};
+  std::vector<Range> out{{C, (size_t)(M * N) * c_elem, "C"}};
+  if (int e = check_ranges(in, out)) return e;
+  g.M = (int)M;
+  g.N = (int)N;
+  g.K = (int)K;
+  g.A = (const bf16_t*)A;
+  g.B[0] = (const bf16_t*)B;
+  return LS_OK;
+}
+
+int ls_gemm_nt(int64_t M, int64_t N, int64_t K, const ls_bf16* A, const ls_bf16* B, ls_bf16* C, void* stream) {
+  ls::GemmArgs g;
+  if (int e = gemm_common(M, N, K, A, B, C, 2, g)) return e;
+  g.lda = K;
+  g.ldb = K;
+  g.C = (bf16_t*)C;
+  g.ldc = N;
+  LS_HIP(ls::gemm(g, (hipStream_t)stream), "gemm_nt");
+  return LS_OK;
+}
+
+int ls_gemm_nn(int64_t M, int64_t N, int64_t K, const ls_bf16* A, const ls_bf16* B, ls_bf16* C, void* stream) {
+  ls::GemmArgs g;
+  if (int e = gemm_common(M, N, K, A, B, C, 2, g)) return e;
+  g.lda = K;
+  g.ldb = N;
+  g.b_kcontig = false;
+  g.C = (bf16_t*)C;
+  g.ldc = N;
+  LS_HIP(ls::gemm(g, (hipStream_t)stream), "gemm_nn");
+  return LS_OK;
+}
+
+int ls_gemm_tn(int64_t M, int64_t N, int64_t K, const ls_bf16* A, const ls_bf16* B, float* C, int accumulate,
+               void* stream) {
+  ls::GemmArgs g;
+  if (int e = gemm_common(M, N, K, A, B, C, 4, g)) return e;
+  g.lda = M;
+  g.a_kcontig = false;
+  g.ldb = N;
+  g.b_kcontig = false;
+  g.epi = ls::EPI_F32;
+  g.F[0] = C;
+  g.ldf = N;
+  g.accumulate = accumulate != 0;
+  LS_HIP(ls::gemm(g, (hipStream_t)stream), "gemm_tn");
+  return LS_OK;
+}
+
+}  // extern "C"

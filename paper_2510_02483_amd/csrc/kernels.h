@@ -1,0 +1,82 @@
+// Internal launch interface between the C ABI layer and the HIP kernels.
+// Every launcher enqueues work on `stream` and returns the launch status.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ls {
+
+typedef uint16_t bf16_t;
+
+// ---- matrix products --------------------------------------------------------
+// C[m,n] = sum_k A(m,k) B(k,n), bf16 operands, fp32 accumulation.
+// A: a_kcontig ? A[m*lda + k] : A[k*lda + m].
+// B: b_kcontig ? row n of B (element k contiguous) : row k of B (element n contiguous).
+//    The rows of B may come from up to three buffers: row index r (n if
+//    b_kcontig, else k) reads seg[s] for the last s with start[s] <= r, at row
+//    r - start[s] of that buffer.
+// With glu set (b_kcontig only), virtual column n maps to gate row (n/128)*64 + n%64
+// when (n/64) is even and to the up row with the same index when odd (seg[0] =
+// gate, seg[1] = up, glu_rows = rows of each).
+enum Epilogue {
+  EPI_BF16 = 0,     // C (bf16) = acc
+  EPI_RESID = 1,    // C (bf16) = acc + R
+  EPI_ROPE = 2,     // C (bf16) = rotate(acc) on columns < rope_cols, acc elsewhere
+  EPI_GLU_FWD = 3,  // gu[m][i] = g, gu[m][I+i] = u, act[m][i] = silu(g) u
+  EPI_GLU_BWD = 4,  // C = dgu: dgu[m][i] = acc u silu'(g), dgu[m][I+i] = acc silu(g)
+  EPI_F32 = 5,      // F (fp32, rows split over up to three buffers) (+)= acc
+};
+
+struct GemmArgs {
+  int M = 0, N = 0, K = 0;
+  const bf16_t* A = nullptr;
+  int64_t lda = 0;
+  bool a_kcontig = true;
+  const bf16_t* B[3] = {nullptr, nullptr, nullptr};
+  int b_start[3] = {0, 1 << 30, 1 << 30};
+  int64_t ldb = 0;
+  bool b_kcontig = true;
+  bool glu = false;
+  int glu_rows = 0;
+  int epi = EPI_BF16;
+  bf16_t* C = nullptr;
+  int64_t ldc = 0;
+  const bf16_t* R = nullptr;      // EPI_RESID, leading dimension ldc
+  const float* rope_cs = nullptr; // EPI_ROPE: [seq][head_dim/2] cos then [seq][head_dim/2] sin
+  int seq = 1, head_dim = 128, rope_cols = 0;
+  bf16_t* act = nullptr;          // EPI_GLU_FWD: [M][I]
+  const bf16_t* gu_in = nullptr;  // EPI_GLU_BWD: saved [M][2I]
+  int glu_I = 0;
+  float* F[3] = {nullptr, nullptr, nullptr};  // EPI_F32
+  int f_start[3] = {0, 1 << 30, 1 << 30};
+  int64_t ldf = 0;
+  int accumulate = 0;
+};
+
+hipError_t gemm(const GemmArgs& a, hipStream_t s);
+
+// ---- RMSNorm ------------------------------------------------------------------
+hipError_t rmsnorm_fwd(int64_t rows, int hidden, float eps, const bf16_t* x, const bf16_t* gamma,
+                       bf16_t* h, float* r, hipStream_t s);
+// Partial buffer of rmsnorm_bwd: rmsnorm_bwd_parts(rows) x hidden floats.
+int rmsnorm_bwd_parts(int64_t rows);
+hipError_t rmsnorm_bwd(int64_t rows, int hidden, const bf16_t* x, const bf16_t* gamma, const float* r,
+                       const bf16_t* dh, const bf16_t* dres, bf16_t* dx, float* dgamma, int accumulate,
+                       float* partial, hipStream_t s);
+
+// ---- RoPE table -------------------------------------------------------------
+// cs[p][i] = cos(p theta^(-2i/d)), cs[seq*d/2 + p*d/2 + i] = sin(...), computed in fp64.
+hipError_t rope_table(int seq, int head_dim, double theta, float* cs, hipStream_t s);
+
+// ---- attention ----------------------------------------------------------------
+struct AttnShape {
+  int batch, seq, nq, nkv, d;
+};
+hipError_t attn_fwd(const AttnShape& sh, const bf16_t* qkv, bf16_t* o, float* lse, hipStream_t s);
+// Workspace layout for attn_bwd: D [batch*nq*seq] fp32, dq_acc [batch*seq*nq*d] fp32.
+size_t attn_bwd_workspace(const AttnShape& sh);
+// rope_cs may be null (no inverse rotation of dq and dk).
+hipError_t attn_bwd(const AttnShape& sh, const bf16_t* qkv, const bf16_t* o, const float* lse,
+                    const bf16_t* dout, bf16_t* dqkv, const float* rope_cs, void* ws, hipStream_t s);
+
+}  // namespace ls

@@ -1,0 +1,213 @@
+// RMSNorm forward / backward (with the residual gradient and a deterministic
+// gain-gradient reduction) and the RoPE cos/sin table.
+//
+// These kernels are bound by HBM bandwidth: each row is read with 16-byte
+// coalesced loads (one wave per row) and reduced with wave shuffles.
+#include "common.h"
+#include "kernels.h"
+
+namespace ls {
+
+namespace {
+
+constexpr int NORM_WAVES = 4;          // waves per workgroup (one row per wave at a time)
+constexpr int BWD_ROWS_PER_BLOCK = 32;  // rows whose gain gradient one workgroup sums
+
+LS_DEV void unpack8(const u32x4 w, float f[8]) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    f[2 * e] = bf_lo(w[e]);
+    f[2 * e + 1] = bf_hi(w[e]);
+  }
+}
+
+LS_DEV u32x4 pack8(const float f[8]) {
+  return u32x4{pack_bf2(f[0], f[1]), pack_bf2(f[2], f[3]), pack_bf2(f[4], f[5]), pack_bf2(f[6], f[7])};
+}
+
+// h = x * r * gamma, r = 1/sqrt(mean(x^2) + eps); CH = ceil(hidden / 512) chunks per lane.
+template <int CH>
+__global__ __launch_bounds__(64 * NORM_WAVES) void rmsnorm_fwd_kernel(int64_t rows, int hidden, float eps,
+                                                                      const bf16_t* __restrict__ x,
+                                                                      const bf16_t* __restrict__ gamma,
+                                                                      bf16_t* __restrict__ h, float* __restrict__ r) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * NORM_WAVES + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const int chunks = hidden / 8;
+  const bf16_t* xr = x + row * hidden;
+  u32x4 xv[CH];
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < CH; ++i) {
+    const int c = lane + 64 * i;
+    xv[i] = c < chunks ? *(const u32x4*)(xr + c * 8) : u32x4{0u, 0u, 0u, 0u};
+    float f[8];
+    unpack8(xv[i], f);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ss += f[e] * f[e];
+  }
+  ss = wave_sum(ss);
+  const float rs = 1.0f / sqrtf(ss / (float)hidden + eps);
+  if (lane == 0) r[row] = rs;
+#pragma unroll
+  for (int i = 0; i < CH; ++i) {
+    const int c = lane + 64 * i;
+    if (c >= chunks) continue;
+    float f[8], g[8];
+    unpack8(xv[i], f);
+    unpack8(*(const u32x4*)(gamma + c * 8), g);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) f[e] = f[e] * rs * g[e];
+    *(u32x4*)(h + row * hidden + c * 8) = pack8(f);
+  }
+}
+
+// dx = dres + r*a - x*r^3*<a,x>/hidden with a = gamma*dh; per-workgroup
+// partial sums of dh*x*r over its rows go to partial[blockIdx.x][hidden].
+template <int CH>
+__global__ __launch_bounds__(64 * NORM_WAVES) void rmsnorm_bwd_kernel(int64_t rows, int hidden,
+                                                                      const bf16_t* __restrict__ x,
+                                                                      const bf16_t* __restrict__ gamma,
+                                                                      const float* __restrict__ r,
+                                                                      const bf16_t* __restrict__ dh,
+                                                                      const bf16_t* __restrict__ dres,
+                                                                      bf16_t* __restrict__ dx,
+                                                                      float* __restrict__ partial) {
+  __shared__ float red[CH * 512];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int chunks = hidden / 8;
+  float gsum[CH][8];
+#pragma unroll
+  for (int i = 0; i < CH; ++i)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) gsum[i][e] = 0.f;
+  const int64_t row_begin = (int64_t)blockIdx.x * BWD_ROWS_PER_BLOCK;
+  for (int rr = wave; rr < BWD_ROWS_PER_BLOCK; rr += NORM_WAVES) {
+    const int64_t row = row_begin + rr;
+    if (row >= rows) break;
+    const float rs = r[row];
+    u32x4 xv[CH], dv[CH];
+    float dot = 0.f;
+#pragma unroll
+    for (int i = 0; i < CH; ++i) {
+      const int c = lane + 64 * i;
+      xv[i] = dv[i] = u32x4{0u, 0u, 0u, 0u};
+      if (c >= chunks) continue;
+      xv[i] = *(const u32x4*)(x + row * hidden + c * 8);
+      dv[i] = *(const u32x4*)(dh + row * hidden + c * 8);
+      float xf[8], df[8], g[8];
+      unpack8(xv[i], xf);
+      unpack8(dv[i], df);
+      unpack8(*(const u32x4*)(gamma + c * 8), g);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        dot += g[e] * df[e] * xf[e];
+        gsum[i][e] += df[e] * xf[e] * rs;
+      }
+    }
+    dot = wave_sum(dot);
+    const float coef = rs * rs * rs * dot / (float)hidden;
+#pragma unroll
+    for (int i = 0; i < CH; ++i) {
+      const int c = lane + 64 * i;
+      if (c >= chunks) continue;
+      float xf[8], df[8], g[8], o[8], rf[8];
+      unpack8(xv[i], xf);
+      unpack8(dv[i], df);
+      unpack8(*(const u32x4*)(gamma + c * 8), g);
+      if (dres) unpack8(*(const u32x4*)(dres + row * hidden + c * 8), rf);
+      else
+#pragma unroll
+        for (int e = 0; e < 8; ++e) rf[e] = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] = rf[e] + rs * g[e] * df[e] - xf[e] * coef;
+      *(u32x4*)(dx + row * hidden + c * 8) = pack8(o);
+    }
+  }
+  // combine the waves' column sums in a fixed order (deterministic)
+  for (int w = 0; w < NORM_WAVES; ++w) {
+    if (wave == w) {
+#pragma unroll
+      for (int i = 0; i < CH; ++i)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int j = (lane + 64 * i) * 8 + e;
+          red[j] = w == 0 ? gsum[i][e] : red[j] + gsum[i][e];
+        }
+    }
+    __syncthreads();
+  }
+  for (int j = threadIdx.x; j < hidden; j += 64 * NORM_WAVES) partial[(int64_t)blockIdx.x * hidden + j] = red[j];
+}
+
+// dgamma[j] (+)= sum over parts of partial[p][j], parts summed in order.
+__global__ void column_sum_kernel(int parts, int hidden, const float* __restrict__ partial,
+                                  float* __restrict__ out, int accumulate) {
+  const int j = blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= hidden) return;
+  float s = 0.f;
+  for (int p = 0; p < parts; ++p) s += partial[(int64_t)p * hidden + j];
+  out[j] = accumulate ? out[j] + s : s;
+}
+
+__global__ void rope_table_kernel(int seq, int head_dim, double theta, float* __restrict__ cs) {
+  const int half = head_dim / 2;
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)seq * half) return;
+  const int p = (int)(idx / half), i = (int)(idx % half);
+  const double ang = (double)p * pow(theta, -2.0 * (double)i / (double)head_dim);
+  cs[idx] = (float)cos(ang);
+  cs[(int64_t)seq * half + idx] = (float)sin(ang);
+}
+
+}  // namespace
+
+hipError_t rmsnorm_fwd(int64_t rows, int hidden, float eps, const bf16_t* x, const bf16_t* gamma, bf16_t* h,
+                       float* r, hipStream_t s) {
+  const int ch = (hidden / 8 + 63) / 64;
+  const dim3 grid((unsigned)((rows + NORM_WAVES - 1) / NORM_WAVES)), block(64 * NORM_WAVES);
+#define LS_F(CHV) \
+  case CHV: hipLaunchKernelGGL((rmsnorm_fwd_kernel<CHV>), grid, block, 0, s, rows, hidden, eps, x, gamma, h, r); break;
+  switch (ch) {
+    LS_F(1) LS_F(2) LS_F(3) LS_F(4) LS_F(5) LS_F(6) LS_F(7) LS_F(8)
+    LS_F(9) LS_F(10) LS_F(11) LS_F(12) LS_F(13) LS_F(14) LS_F(15) LS_F(16)
+    default: return hipErrorInvalidValue;
+  }
+#undef LS_F
+  return hipGetLastError();
+}
+
+int rmsnorm_bwd_parts(int64_t rows) { return (int)((rows + BWD_ROWS_PER_BLOCK - 1) / BWD_ROWS_PER_BLOCK); }
+
+hipError_t rmsnorm_bwd(int64_t rows, int hidden, const bf16_t* x, const bf16_t* gamma, const float* r,
+                       const bf16_t* dh, const bf16_t* dres, bf16_t* dx, float* dgamma, int accumulate,
+                       float* partial, hipStream_t s) {
+  const int ch = (hidden / 8 + 63) / 64;
+  const int parts = rmsnorm_bwd_parts(rows);
+  const dim3 grid((unsigned)parts), block(64 * NORM_WAVES);
+#define LS_B(CHV)                                                                                       \
+  case CHV:                                                                                             \
+    hipLaunchKernelGGL((rmsnorm_bwd_kernel<CHV>), grid, block, 0, s, rows, hidden, x, gamma, r, dh, dres, dx, \
+                       partial);                                                                        \
+    break;
+  switch (ch) {
+    LS_B(1) LS_B(2) LS_B(3) LS_B(4) LS_B(5) LS_B(6) LS_B(7) LS_B(8)
+    LS_B(9) LS_B(10) LS_B(11) LS_B(12) LS_B(13) LS_B(14) LS_B(15) LS_B(16)
+    default: return hipErrorInvalidValue;
+  }
+#undef LS_B
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(column_sum_kernel, dim3((hidden + 255) / 256), dim3(256), 0, s, parts, hidden,
+                     (const float*)partial, dgamma, accumulate);
+  return hipGetLastError();
+}
+
+hipError_t rope_table(int seq, int head_dim, double theta, float* cs, hipStream_t s) {
+  const int64_t n = (int64_t)seq * (head_dim / 2);
+  hipLaunchKernelGGL(rope_table_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, seq, head_dim, theta, cs);
+  return hipGetLastError();
+}
+
+}  // namespace ls

@@ -1,0 +1,249 @@
+"""Python binding of the C ABI in include/ls.h (ctypes; argument marshalling only).
+
+Every compute step runs in the HIP kernels of libls.so.  torch is used for
+device memory and the current stream.  If libls.so has not been built this
+module raises on first use; there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+from .configs import BlockConfig
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libls.so")
+
+STATUS = {0: "LS_OK", 1: "LS_ERR_NULL", 2: "LS_ERR_SHAPE", 3: "LS_ERR_UNSUPPORTED", 4: "LS_ERR_ALIGN",
+          5: "LS_ERR_ALIAS", 6: "LS_ERR_WORKSPACE", 7: "LS_ERR_HIP"}
+WEIGHTS = ("attn_norm", "wq", "wk", "wv", "wo", "mlp_norm", "wg", "wu", "wd")
+
+
+class LsError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        super().__init__(f"{where}: {STATUS.get(status, status)}: {detail}")
+        self.status = status
+
+
+class LsBlockCfg(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("seq", ctypes.c_int32), ("hidden", ctypes.c_int32),
+                ("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("intermediate", ctypes.c_int32), ("rope_theta", ctypes.c_float), ("rms_eps", ctypes.c_float)]
+
+
+class LsBlockWeights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in WEIGHTS]
+
+
+class LsBlockGrads(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in WEIGHTS]
+
+
+class LsSizes(ctypes.Structure):
+    _fields_ = [("attn_saved", ctypes.c_size_t), ("mlp_saved", ctypes.c_size_t),
+                ("attn_workspace", ctypes.c_size_t), ("mlp_workspace", ctypes.c_size_t),
+                ("block_workspace", ctypes.c_size_t)]
+
+
+_lib = None
+_P = ctypes.c_void_p
+_PROTOS = {
+    "ls_version": (ctypes.c_int, []),
+    "ls_last_error": (ctypes.c_char_p, []),
+    "ls_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "ls_query_sizes": (ctypes.c_int, [_P, _P]),
+    "ls_attn_fwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "ls_attn_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, ctypes.c_int, _P, ctypes.c_size_t, _P]),
+    "ls_mlp_fwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "ls_mlp_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, ctypes.c_int, _P, ctypes.c_size_t, _P]),
+    "ls_block_fwd_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, ctypes.c_int, _P, ctypes.c_size_t, _P]),
+    "ls_attn_core_fwd": (ctypes.c_int, [_P, _P, _P, _P, _P]),
+    "ls_attn_core_bwd_workspace": (ctypes.c_size_t, [_P]),
+    "ls_attn_core_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "ls_rmsnorm_fwd": (ctypes.c_int, [ctypes.c_int64, ctypes.c_int32, ctypes.c_float, _P, _P, _P, _P, _P]),
+    "ls_rmsnorm_bwd_workspace": (ctypes.c_size_t, [ctypes.c_int64, ctypes.c_int32]),
+    "ls_rmsnorm_bwd": (ctypes.c_int, [ctypes.c_int64, ctypes.c_int32, _P, _P, _P, _P, _P, _P, _P, ctypes.c_int, _P,
+                                      ctypes.c_size_t, _P]),
+    "ls_gemm_nt": (ctypes.c_int, [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, _P, _P, _P, _P]),
+    "ls_gemm_nn": (ctypes.c_int, [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, _P, _P, _P, _P]),
+    "ls_gemm_tn": (ctypes.c_int, [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, _P, _P, _P, ctypes.c_int, _P]),
+    "ls_timing_begin": (ctypes.c_int, [ctypes.c_char_p, ctypes.c_int]),
+    "ls_timing_end": (ctypes.c_int, [_P, _P]),
+}
+EXPORTS = tuple(_PROTOS)
+
+
+def lib():
+    """Load libls.so (after torch, so that both share one HIP runtime)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2510_02483_amd.build`")
+        l = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _PROTOS.items():
+            f = getattr(l, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = l
+    return _lib
+
+
+def _check(status: int, where: str):
+    if status != 0:
+        raise LsError(status, where, lib().ls_last_error().decode())
+
+
+def _p(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def make_cfg(c: BlockConfig) -> LsBlockCfg:
+    return LsBlockCfg(c.batch, c.seq, c.hidden, c.n_q_heads, c.n_kv_heads, c.head_dim, c.intermediate,
+                      c.rope_theta, c.rms_eps)
+
+
+def make_weights(w: dict) -> LsBlockWeights:
+    return LsBlockWeights(*[w[n].data_ptr() if w.get(n) is not None else None for n in WEIGHTS])
+
+
+def make_grads(g: dict) -> LsBlockGrads:
+    return LsBlockGrads(*[g[n].data_ptr() if g.get(n) is not None else None for n in WEIGHTS])
+
+
+# ---- the ABI calls, same names ----------------------------------------------------
+
+def ls_version() -> int:
+    return lib().ls_version()
+
+
+def ls_query_sizes(c: BlockConfig) -> dict:
+    s = LsSizes()
+    cfg = make_cfg(c)
+    _check(lib().ls_query_sizes(ctypes.byref(cfg), ctypes.byref(s)), "ls_query_sizes")
+    return {n: getattr(s, n) for n, _ in LsSizes._fields_}
+
+
+def ls_attn_fwd(c, x, w, x2, attn_saved, workspace, stream=None):
+    cfg, wt = make_cfg(c), make_weights(w)
+    _check(lib().ls_attn_fwd(ctypes.byref(cfg), _p(x), ctypes.byref(wt), _p(x2), _p(attn_saved), _p(workspace),
+                             workspace.numel() * workspace.element_size(), _stream(stream)), "ls_attn_fwd")
+
+
+def ls_attn_bwd(c, x, w, attn_saved, dx2, dx, grads, accumulate, workspace, stream=None):
+    cfg, wt, gr = make_cfg(c), make_weights(w), make_grads(grads)
+    _check(lib().ls_attn_bwd(ctypes.byref(cfg), _p(x), ctypes.byref(wt), _p(attn_saved), _p(dx2), _p(dx),
+                             ctypes.byref(gr), int(accumulate), _p(workspace),
+                             workspace.numel() * workspace.element_size(), _stream(stream)), "ls_attn_bwd")
+
+
+def ls_mlp_fwd(c, x2, w, y, mlp_saved, workspace=None, stream=None):
+    cfg, wt = make_cfg(c), make_weights(w)
+    nb = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().ls_mlp_fwd(ctypes.byref(cfg), _p(x2), ctypes.byref(wt), _p(y), _p(mlp_saved), _p(workspace), nb,
+                            _stream(stream)), "ls_mlp_fwd")
+
+
+def ls_mlp_bwd(c, x2, w, mlp_saved, dy, dx2, grads, accumulate, workspace, stream=None):
+    cfg, wt, gr = make_cfg(c), make_weights(w), make_grads(grads)
+    _check(lib().ls_mlp_bwd(ctypes.byref(cfg), _p(x2), ctypes.byref(wt), _p(mlp_saved), _p(dy), _p(dx2),
+                            ctypes.byref(gr), int(accumulate), _p(workspace),
+                            workspace.numel() * workspace.element_size(), _stream(stream)), "ls_mlp_bwd")
+
+
+def ls_block_fwd_bwd(c, x, w, dy, y, dx, grads, accumulate, workspace, stream=None):
+    cfg, wt, gr = make_cfg(c), make_weights(w), make_grads(grads)
+    _check(lib().ls_block_fwd_bwd(ctypes.byref(cfg), _p(x), ctypes.byref(wt), _p(dy), _p(y), _p(dx),
+                                  ctypes.byref(gr), int(accumulate), _p(workspace),
+                                  workspace.numel() * workspace.element_size(), _stream(stream)), "ls_block_fwd_bwd")
+
+
+def ls_attn_core_fwd(c, qkv, o, lse, stream=None):
+    cfg = make_cfg(c)
+    _check(lib().ls_attn_core_fwd(ctypes.byref(cfg), _p(qkv), _p(o), _p(lse), _stream(stream)), "ls_attn_core_fwd")
+
+
+def ls_attn_core_bwd_workspace(c) -> int:
+    cfg = make_cfg(c)
+    return lib().ls_attn_core_bwd_workspace(ctypes.byref(cfg))
+
+
+def ls_attn_core_bwd(c, qkv, o, lse, dout, dqkv, workspace, stream=None):
+    cfg = make_cfg(c)
+    _check(lib().ls_attn_core_bwd(ctypes.byref(cfg), _p(qkv), _p(o), _p(lse), _p(dout), _p(dqkv), _p(workspace),
+                                  workspace.numel() * workspace.element_size(), _stream(stream)), "ls_attn_core_bwd")
+
+
+def ls_rmsnorm_fwd(rows, hidden, eps, x, gamma, h, r, stream=None):
+    _check(lib().ls_rmsnorm_fwd(rows, hidden, eps, _p(x), _p(gamma), _p(h), _p(r), _stream(stream)), "ls_rmsnorm_fwd")
+
+
+def ls_rmsnorm_bwd_workspace(rows, hidden) -> int:
+    return lib().ls_rmsnorm_bwd_workspace(rows, hidden)
+
+
+def ls_rmsnorm_bwd(rows, hidden, x, gamma, r, dh, dres, dx, dgamma, accumulate, workspace, stream=None):
+    _check(lib().ls_rmsnorm_bwd(rows, hidden, _p(x), _p(gamma), _p(r), _p(dh), _p(dres), _p(dx), _p(dgamma),
+                                int(accumulate), _p(workspace), workspace.numel() * workspace.element_size(),
+                                _stream(stream)), "ls_rmsnorm_bwd")
+
+
+def ls_gemm_nt(A, B, C, stream=None):
+    M, K = A.shape
+    N = B.shape[0]
+    _check(lib().ls_gemm_nt(M, N, K, _p(A), _p(B), _p(C), _stream(stream)), "ls_gemm_nt")
+
+
+def ls_gemm_nn(A, B, C, stream=None):
+    M, K = A.shape
+    N = B.shape[1]
+    _check(lib().ls_gemm_nn(M, N, K, _p(A), _p(B), _p(C), _stream(stream)), "ls_gemm_nn")
+
+
+def ls_gemm_tn(A, B, C, accumulate=False, stream=None):
+    K, M = A.shape
+    N = B.shape[1]
+    _check(lib().ls_gemm_tn(M, N, K, _p(A), _p(B), _p(C), int(accumulate), _stream(stream)), "ls_gemm_tn")
+
+
+def ls_timing_begin(label: str, max_launches: int):
+    _check(lib().ls_timing_begin(label.encode(), int(max_launches)), "ls_timing_begin")
+
+
+def ls_timing_end():
+    """Returns (number of recorded launches, mean milliseconds)."""
+    n = ctypes.c_int(0)
+    ms = ctypes.c_float(0.0)
+    _check(lib().ls_timing_end(ctypes.byref(n), ctypes.byref(ms)), "ls_timing_end")
+    return n.value, ms.value
+
+
+# ---- a small harness around ls_block_fwd_bwd ------------------------------------------
+
+class Block:
+    """Device buffers for one configuration plus a call of ls_block_fwd_bwd.
+
+    Inputs are bf16 CPU tensors from inputs.make_inputs; they are copied to the
+    device once.  Gradients are fp32 device tensors."""
+
+    def __init__(self, c: BlockConfig, host_inputs: dict, device="cuda"):
+        self.cfg = c
+        dev = torch.device(device)
+        self.x = host_inputs["x"].to(dev).reshape(c.tokens, c.hidden).contiguous()
+        self.dy = host_inputs["dy"].to(dev).reshape(c.tokens, c.hidden).contiguous()
+        self.w = {n: host_inputs[n].to(dev).contiguous() for n in WEIGHTS}
+        self.grads = {n: torch.zeros(self.w[n].shape, dtype=torch.float32, device=dev) for n in WEIGHTS}
+        self.y = torch.empty_like(self.x)
+        self.dx = torch.empty_like(self.x)
+        sizes = ls_query_sizes(c)
+        self.workspace = torch.empty(sizes["block_workspace"], dtype=torch.uint8, device=dev)
+
+    def step(self, accumulate=False, stream=None):
+        ls_block_fwd_bwd(self.cfg, self.x, self.w, self.dy, self.y, self.dx, self.grads, accumulate,
+                         self.workspace, stream)

@@ -1,0 +1,122 @@
+"""The C ABI library: it loads, exports every symbol include/ls.h declares, and
+rejects bad arguments before touching the GPU (these run on a host with no GPU;
+no call here reaches a HIP API)."""
+import ctypes
+import os
+import re
+
+import pytest
+import torch  # noqa: F401  (load torch's HIP runtime first, as the binding does)
+
+from paper_2510_02483_amd import configs, lib as L
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "ls.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(L.LIB_PATH), reason="libls.so not built")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ls_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol():
+    names = declared_functions()
+    assert len(names) >= 18
+    lib = ctypes.CDLL(L.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(L.EXPORTS), "binding and header disagree"
+
+
+def test_version_and_status_strings():
+    assert L.ls_version() == 100
+    for code in range(8):
+        assert L.lib().ls_status_string(code).decode()
+    assert L.lib().ls_status_string(99).decode() == "unknown status"
+
+
+def cfg_of(c):
+    return L.make_cfg(c)
+
+
+def test_query_sizes_tiny():
+    s = L.ls_query_sizes(configs.TINY)
+    c = configs.TINY
+    T, H, I = c.tokens, c.hidden, c.intermediate
+    # saved state holds at least h1, qkv, o (bf16) and r1, lse (fp32)
+    assert s["attn_saved"] >= 2 * T * (H + c.dq + 2 * c.dkv + c.dq) + 4 * (T + c.batch * c.n_q_heads * c.seq)
+    assert s["mlp_saved"] >= 2 * T * (H + 3 * I) + 4 * T
+    assert s["block_workspace"] >= s["attn_saved"] + s["mlp_saved"] + 4 * T * H
+    assert all(v % 256 == 0 for v in s.values())
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("batch", 0, 2), ("seq", -1, 2), ("hidden", 0, 2), ("n_kv_heads", 3, 2),
+    ("hidden", 260, 2), ("intermediate", 690, 2), ("head_dim", 96, 3), ("head_dim", 32, 3),
+    ("rope_theta", 1.0, 2), ("rms_eps", -1e-5, 2), ("hidden", 16384, 3),
+])
+def test_query_sizes_rejects(field, value, status):
+    c = configs.TINY.with_(**{field: value})
+    with pytest.raises(L.LsError) as e:
+        L.ls_query_sizes(c)
+    assert e.value.status == status
+
+
+def test_null_pointers():
+    lib = L.lib()
+    s = L.LsSizes()
+    assert lib.ls_query_sizes(None, ctypes.byref(s)) == 1
+    cfg = cfg_of(configs.TINY)
+    assert lib.ls_query_sizes(ctypes.byref(cfg), None) == 1
+    assert lib.ls_attn_fwd(ctypes.byref(cfg), None, None, None, None, None, 0, None) == 1
+    w = L.LsBlockWeights()
+    assert lib.ls_attn_fwd(ctypes.byref(cfg), ctypes.c_void_p(4096), ctypes.byref(w), ctypes.c_void_p(1 << 40),
+                           ctypes.c_void_p(1 << 41), ctypes.c_void_p(1 << 42), 1 << 30, None) == 1
+    assert "NULL" in lib.ls_last_error().decode()
+
+
+def _fake_weights(c, base=1 << 36, stride=1 << 30):
+    return L.LsBlockWeights(*[base + i * stride for i in range(9)])
+
+
+def _fake_grads(c, base=1 << 44, stride=1 << 30):
+    return L.LsBlockGrads(*[base + i * stride for i in range(9)])
+
+
+def test_alignment_alias_and_workspace():
+    lib = L.lib()
+    c = configs.TINY
+    cfg = cfg_of(c)
+    sizes = L.ls_query_sizes(c)
+    w, g = _fake_weights(c), _fake_grads(c)
+    x, dy, y, dx, ws = (1 << 32), (1 << 33), (1 << 34), (1 << 35), (1 << 46)
+    V = ctypes.c_void_p
+    call = lambda x_, dy_, y_, dx_, ws_, n: lib.ls_block_fwd_bwd(  # noqa: E731
+        ctypes.byref(cfg), V(x_), ctypes.byref(w), V(dy_), V(y_), V(dx_), ctypes.byref(g), 0, V(ws_), n, None)
+    assert call(x + 2, dy, y, dx, ws, sizes["block_workspace"]) == 4  # misaligned
+    assert call(x, dy, x, dx, ws, sizes["block_workspace"]) == 5      # y aliases x
+    assert call(x, dy, y, y + 64, ws, sizes["block_workspace"]) == 5  # dx overlaps y
+    assert call(x, dy, y, dx, ws, sizes["block_workspace"] - 256) == 6
+    assert "workspace" in lib.ls_last_error().decode()
+    # gradient buffer overlapping an input
+    g2 = _fake_grads(c)
+    g2.wq = x
+    assert lib.ls_block_fwd_bwd(ctypes.byref(cfg), V(x), ctypes.byref(w), V(dy), V(y), V(dx), ctypes.byref(g2), 0,
+                                V(ws), sizes["block_workspace"], None) == 5
+
+
+def test_gemm_and_norm_argument_checks():
+    lib = L.lib()
+    V = ctypes.c_void_p
+    assert lib.ls_gemm_nt(0, 8, 8, V(1 << 32), V(1 << 33), V(1 << 34), None) == 2
+    assert lib.ls_gemm_nt(12, 8, 8, V(1 << 32), V(1 << 33), V(1 << 34), None) == 2
+    assert lib.ls_gemm_nn(8, 8, 8, V(1 << 32), V((1 << 33) + 8), V(1 << 34), None) == 4
+    assert lib.ls_gemm_tn(64, 64, 64, V(1 << 32), V(1 << 33), V(1 << 32), 0, None) == 5
+    assert lib.ls_rmsnorm_fwd(4, 12, 1e-5, V(1 << 32), V(1 << 33), V(1 << 34), V(1 << 35), None) == 2
+    assert lib.ls_rmsnorm_fwd(4, 16, -1.0, V(1 << 32), V(1 << 33), V(1 << 34), V(1 << 35), None) == 2
+    need = lib.ls_rmsnorm_bwd_workspace(100, 64)
+    assert need >= 64 * 4
+    assert lib.ls_rmsnorm_bwd(100, 64, V(1 << 32), V(1 << 33), V(1 << 34), V(1 << 35), None, V(1 << 36),
+                              V(1 << 37), 0, V(1 << 38), need - 4, None) == 6
