@@ -108,8 +108,11 @@ int check_cfg(const ls_block_cfg* c) {
   if (c->hidden > 8192) return fail(LS_ERR_UNSUPPORTED, "hidden %d exceeds 8192", c->hidden);
   const Dims m = dims_of(*c);
   const int64_t lim = (int64_t)1 << 30;
-  if (m.T >= lim || m.Dqkv >= lim || 2 * m.I >= lim || m.T * std::max<int64_t>(m.Dqkv, 2 * m.I) >= ((int64_t)1 << 40))
-    return fail(LS_ERR_SHAPE, "problem too large");
+  // every matrix is addressed with 32-bit byte offsets (buffer loads)
+  const int64_t widest = std::max(std::max(m.Dqkv, 2 * m.I), m.H);
+  if (m.T >= lim || m.Dqkv >= lim || 2 * m.I >= lim || m.T * widest * 2 >= ((int64_t)1 << 31) ||
+      m.I * m.H * 2 >= ((int64_t)1 << 31) || m.Dqkv * m.H * 2 >= ((int64_t)1 << 31))
+    return fail(LS_ERR_SHAPE, "problem too large (a matrix reaches 2 GiB)");
   return LS_OK;
 }
 
@@ -815,6 +818,8 @@ static int check_gemm(int64_t M, int64_t N, int64_t K) {
   if (M <= 0 || N <= 0 || K <= 0) return fail(LS_ERR_SHAPE, "M, N, K must be positive");
   if (M % 8 || N % 8 || K % 8) return fail(LS_ERR_SHAPE, "M, N, K must be multiples of 8");
   if (M >= (1 << 30) || N >= (1 << 30) || K >= (1 << 30)) return fail(LS_ERR_SHAPE, "dimension too large");
+  if (M * K * 2 >= ((int64_t)1 << 31) || K * N * 2 >= ((int64_t)1 << 31) || M * N * 4 >= ((int64_t)1 << 31))
+    return fail(LS_ERR_SHAPE, "an operand reaches 2 GiB");
   return LS_OK;
 }
 

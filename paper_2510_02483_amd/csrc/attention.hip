@@ -15,14 +15,16 @@
 // loads in the key order the probabilities arrive in.  The softmax runs in
 // base 2 with the 1/sqrt(d) scale folded into one multiplier.
 //
-// Backward (one workgroup = 128 keys of one kv head, 4 waves x 32 keys): the
-// workgroup loops over the query heads of its group and over 64-row query
-// tiles from the diagonal on; per tile it recomputes S = Q K^T and dP = dO V^T
-// with keys as MFMA columns (a lane owns one key), forms P and dS = P (dP - D)
-// in registers and accumulates dV^T += dO^T P and dK^T += Q^T dS there (the sum
-// over the group's query heads happens in the same registers).  dS goes to
-// LDS once so that dQ = dS K can be formed and added into an fp32 buffer with
-// atomics; a last pass scales, un-rotates and converts dQ.
+// Backward, two kernels and no atomics.  dK/dV (one workgroup = 128 keys of
+// one kv head, 4 waves x 32 keys): the workgroup loops over the query heads of
+// its group and over 64-row query tiles from the diagonal on; per tile it
+// recomputes S = Q K^T and dP = dO V^T with keys as MFMA columns (a lane owns
+// one key), forms P and dS = P (dP - D) in registers and accumulates
+// dV^T += dO^T P and dK^T += Q^T dS there (the sum over the group's query heads
+// happens in the same registers).  dQ (one workgroup = 128 queries of one
+// head): loops over key tiles like the forward, recomputing S^T and dP^T, and
+// accumulates dQ^T += K^T dS^T.  Both kernels write their gradient already
+// scaled and un-rotated (inverse RoPE) in bf16.
 #include <math.h>
 
 #include "common.h"
@@ -184,11 +186,10 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnShape sh, const bf
   }
 }
 
-// D[b,h,s] = <dO, O> over the head's d columns; also zeroes the fp32 dQ buffer.
+// D[b,h,s] = <dO, O> over the head's d columns (fp32).
 template <int D>
 __global__ __launch_bounds__(256) void attn_bwd_pre_kernel(AttnShape sh, const bf16_t* __restrict__ o,
-                                                           const bf16_t* __restrict__ dout, float* __restrict__ Dv,
-                                                           float* __restrict__ dq_acc) {
+                                                           const bf16_t* __restrict__ dout, float* __restrict__ Dv) {
   constexpr int CPH = D / 8;  // 16-byte chunks per head
   const int lane = threadIdx.x & 63;
   const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -197,7 +198,6 @@ __global__ __launch_bounds__(256) void attn_bwd_pre_kernel(AttnShape sh, const b
   const int chunks = sh.nq * CPH;
   const bf16_t* orow = o + t * sh.nq * D;
   const bf16_t* drow = dout + t * sh.nq * D;
-  float* qrow = dq_acc + t * sh.nq * D;
   for (int c0 = 0; c0 < chunks; c0 += 64) {
     const int c = c0 + lane;
     float acc = 0.f;
@@ -205,9 +205,6 @@ __global__ __launch_bounds__(256) void attn_bwd_pre_kernel(AttnShape sh, const b
       const u32x4 a = load16(orow + c * 8), g = load16(drow + c * 8);
 #pragma unroll
       for (int e = 0; e < 4; ++e) acc += bf_lo(a[e]) * bf_lo(g[e]) + bf_hi(a[e]) * bf_hi(g[e]);
-      const f32x4 z = {0.f, 0.f, 0.f, 0.f};
-      *(f32x4*)(qrow + c * 8) = z;
-      *(f32x4*)(qrow + c * 8 + 4) = z;
     }
 #pragma unroll
     for (int off = CPH / 2; off >= 1; off >>= 1) acc += __shfl_xor(acc, off);
@@ -215,20 +212,55 @@ __global__ __launch_bounds__(256) void attn_bwd_pre_kernel(AttnShape sh, const b
   }
 }
 
+// Inverse rotation of a gradient held in MFMA layout: lane holds columns
+// 32i + 8(r/4) + 4lh + r%4 of one row at position `pos`; the pair partner of
+// column d < D/2 is d + D/2, in register block i + D/64 of the same lane.
 template <int D>
-__global__ __launch_bounds__(256, 1) void attn_bwd_kernel(AttnShape sh, const bf16_t* __restrict__ qkv,
-                                                           const bf16_t* __restrict__ dout,
-                                                           const float* __restrict__ lse,
-                                                           const float* __restrict__ Dv, float* __restrict__ dq_acc,
-                                                           bf16_t* __restrict__ dqkv, const float* __restrict__ rope_cs,
-                                                           float scale, float sl2) {
-  constexpr int QP = D + 8, TP = BWD_BQ + 8, SP = BWD_BKV + 8;
+LS_DEV void unrotate_store(const f32x16 (&acc)[D / 32], float scale, const float* rope_cs, int seq, int pos, int lh,
+                           bf16_t* row) {
+  constexpr int HALF = D / 2, IP = HALF / 32;
+#pragma unroll
+  for (int i = 0; i < D / 32; ++i)
+#pragma unroll
+    for (int rq = 0; rq < 4; ++rq) {
+      const int d = 32 * i + 8 * rq + 4 * lh;
+      float out[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float x = acc[i][4 * rq + e] * scale;
+        if (rope_cs == nullptr) {
+          out[e] = x;
+        } else if (i < IP) {  // first half: x1' = x1 cos + x2 sin
+          const float x2 = acc[i + IP][4 * rq + e] * scale;
+          const float c = rope_cs[(int64_t)pos * HALF + d + e];
+          const float sn = rope_cs[(int64_t)seq * HALF + (int64_t)pos * HALF + d + e];
+          out[e] = x * c + x2 * sn;
+        } else {  // second half: x2' = x2 cos - x1 sin
+          const float x1 = acc[i - IP][4 * rq + e] * scale;
+          const int dl = d - HALF + e;
+          const float c = rope_cs[(int64_t)pos * HALF + dl];
+          const float sn = rope_cs[(int64_t)seq * HALF + (int64_t)pos * HALF + dl];
+          out[e] = x * c - x1 * sn;
+        }
+      }
+      *(u32x2*)(row + d) = u32x2{pack_bf2(out[0], out[1]), pack_bf2(out[2], out[3])};
+    }
+}
+
+// dK and dV for 128 keys of one kv head (4 waves x 32 keys), summed over the
+// query heads of the group, no atomics.
+template <int D>
+__global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnShape sh, const bf16_t* __restrict__ qkv,
+                                                                const bf16_t* __restrict__ dout,
+                                                                const float* __restrict__ lse,
+                                                                const float* __restrict__ Dv, bf16_t* __restrict__ dqkv,
+                                                                const float* __restrict__ rope_cs, float scale,
+                                                                float sl2) {
+  constexpr int QP = D + 8, TP = BWD_BQ + 8;
   __shared__ __attribute__((aligned(16))) bf16_t Qs[BWD_BQ * QP];
   __shared__ __attribute__((aligned(16))) bf16_t dOs[BWD_BQ * QP];
   __shared__ __attribute__((aligned(16))) bf16_t Qt[D * TP];
   __shared__ __attribute__((aligned(16))) bf16_t dOt[D * TP];
-  __shared__ __attribute__((aligned(16))) bf16_t dSs[BWD_BQ * SP];
-  __shared__ __attribute__((aligned(16))) bf16_t Kt[D * SP];
   __shared__ __attribute__((aligned(16))) float lse_s[BWD_BQ];
   __shared__ __attribute__((aligned(16))) float D_s[BWD_BQ];
 
@@ -249,7 +281,6 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kernel(AttnShape sh, const bf
     kf[s] = ok ? load16(base + (int64_t)kvrow * ld + (nq + kvh) * D + 16 * s + 8 * lh) : u32x4{0u, 0u, 0u, 0u};
     vf[s] = ok ? load16(base + (int64_t)kvrow * ld + (nq + nkv + kvh) * D + 16 * s + 8 * lh) : u32x4{0u, 0u, 0u, 0u};
   }
-  stage_transposed<BWD_BKV, D, SP, 256>(Kt, base, ld, kv0, S, (nq + kvh) * D, tid);
 
   f32x16 dk[D / 32], dv[D / 32];
 #pragma unroll
@@ -274,154 +305,141 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kernel(AttnShape sh, const bf
         D_s[tid] = q < S ? D_h[q] : 0.f;
       }
       __syncthreads();
+      if (kv0 + 32 * wave > q0 + BWD_BQ - 1) continue;  // every query of the tile precedes this wave's keys
 
-      const bool active = kv0 + 32 * wave <= q0 + BWD_BQ - 1;
-      if (active) {
-        f32x16 sacc[2], pacc[2];
+      f32x16 sacc[2], pacc[2];
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
+      for (int qb = 0; qb < 2; ++qb) {
 #pragma unroll
-          for (int r = 0; r < 16; ++r) sacc[qb][r] = pacc[qb][r] = 0.f;
+        for (int r = 0; r < 16; ++r) sacc[qb][r] = pacc[qb][r] = 0.f;
 #pragma unroll
-          for (int s = 0; s < D / 16; ++s) {
-            sacc[qb] = mfma32(load16(&Qs[(32 * qb + lr) * QP + 16 * s + 8 * lh]), kf[s], sacc[qb]);
-            pacc[qb] = mfma32(load16(&dOs[(32 * qb + lr) * QP + 16 * s + 8 * lh]), vf[s], pacc[qb]);
-          }
+        for (int s = 0; s < D / 16; ++s) {
+          sacc[qb] = mfma32(load16(&Qs[(32 * qb + lr) * QP + 16 * s + 8 * lh]), kf[s], sacc[qb]);
+          pacc[qb] = mfma32(load16(&dOs[(32 * qb + lr) * QP + 16 * s + 8 * lh]), vf[s], pacc[qb]);
         }
-        // lane holds key kvrow, queries q0 + 32qb + 8(r/4) + 4lh + r%4
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-          for (int rq = 0; rq < 4; ++rq) {
-            const int ql = 32 * qb + 8 * rq + 4 * lh;
-            const f32x4 L = *(const f32x4*)&lse_s[ql];
-            const f32x4 Dd = *(const f32x4*)&D_s[ql];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const int r = 4 * rq + e, q = q0 + ql + e;
-              const float p = (kvrow <= q && q < S) ? exp2f(sacc[qb][r] * sl2 - L[e]) : 0.f;
-              pacc[qb][r] = p * (pacc[qb][r] - Dd[e]);
-              sacc[qb][r] = p;
-            }
-          }
-#pragma unroll
-        for (int s = 0; s < BWD_BQ / 16; ++s) {
-          const u32x4 pf = pack_frag(sacc[s >> 1], 8 * (s & 1));
-          const u32x4 sf = pack_frag(pacc[s >> 1], 8 * (s & 1));
-#pragma unroll
-          for (int i = 0; i < D / 32; ++i) {
-            dv[i] = mfma32(ld_pair8(&dOt[(32 * i + lr) * TP + 16 * s + 4 * lh]), pf, dv[i]);
-            dk[i] = mfma32(ld_pair8(&Qt[(32 * i + lr) * TP + 16 * s + 4 * lh]), sf, dk[i]);
-          }
-        }
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int ql = 32 * qb + 8 * (r >> 2) + 4 * lh + (r & 3);
-            dSs[ql * SP + 32 * wave + lr] = (bf16_t)f2bf(pacc[qb][r]);
-          }
-      } else {
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int ql = 32 * qb + 8 * (r >> 2) + 4 * lh + (r & 3);
-            dSs[ql * SP + 32 * wave + lr] = 0;
-          }
       }
-      __syncthreads();
-
-      // dQ^T[d][q] = K^T[d][:] dS^T[:][q] over the workgroup's keys
-      for (int pr = wave; pr < 2 * (D / 32); pr += 4) {
-        const int qb = pr & 1, db = pr >> 1;
-        f32x16 acc;
+      // lane holds key kvrow, queries q0 + 32qb + 8(r/4) + 4lh + r%4
 #pragma unroll
-        for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+      for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
-        for (int s = 0; s < BWD_BKV / 16; ++s)
-          acc = mfma32(load16(&Kt[(32 * db + lr) * SP + 16 * s + 8 * lh]),
-                       load16(&dSs[(32 * qb + lr) * SP + 16 * s + 8 * lh]), acc);
-        const int q = q0 + 32 * qb + lr;
-        if (q < S) {
-          float* dst = dq_acc + (((int64_t)b * S + q) * nq + h) * D + 32 * db + 4 * lh;
+        for (int rq = 0; rq < 4; ++rq) {
+          const int ql = 32 * qb + 8 * rq + 4 * lh;
+          const f32x4 L = *(const f32x4*)&lse_s[ql];
+          const f32x4 Dd = *(const f32x4*)&D_s[ql];
 #pragma unroll
-          for (int r = 0; r < 16; ++r) atomicAdd(dst + 8 * (r >> 2) + (r & 3), acc[r]);
+          for (int e = 0; e < 4; ++e) {
+            const int r = 4 * rq + e, q = q0 + ql + e;
+            const float p = (kvrow <= q && q < S) ? exp2f(sacc[qb][r] * sl2 - L[e]) : 0.f;
+            pacc[qb][r] = p * (pacc[qb][r] - Dd[e]);
+            sacc[qb][r] = p;
+          }
+        }
+#pragma unroll
+      for (int s = 0; s < BWD_BQ / 16; ++s) {
+        const u32x4 pf = pack_frag(sacc[s >> 1], 8 * (s & 1));
+        const u32x4 sf = pack_frag(pacc[s >> 1], 8 * (s & 1));
+#pragma unroll
+        for (int i = 0; i < D / 32; ++i) {
+          dv[i] = mfma32(ld_pair8(&dOt[(32 * i + lr) * TP + 16 * s + 4 * lh]), pf, dv[i]);
+          dk[i] = mfma32(ld_pair8(&Qt[(32 * i + lr) * TP + 16 * s + 4 * lh]), sf, dk[i]);
         }
       }
     }
   }
 
-  // dK = scale * dS^T Q, un-rotated; dV = P^T dO.  Lane holds key kvrow, columns
-  // 32i + 8(r/4) + 4lh + r%4.
+  // dK = scale * dS^T Q (un-rotated), dV = P^T dO.  Lane holds key kvrow.
   if (kvrow >= S) return;
-  bf16_t* krow = dqkv + ((int64_t)b * S + kvrow) * ld + (nq + kvh) * D;
-  bf16_t* vrow = dqkv + ((int64_t)b * S + kvrow) * ld + (nq + nkv + kvh) * D;
-  constexpr int HALF = D / 2, IP = HALF / 32;
+  const int pos = kvrow;
+  unrotate_store<D>(dk, scale, rope_cs, S, pos, lh, dqkv + ((int64_t)b * S + kvrow) * ld + (nq + kvh) * D);
+  unrotate_store<D>(dv, 1.0f, nullptr, S, pos, lh, dqkv + ((int64_t)b * S + kvrow) * ld + (nq + nkv + kvh) * D);
+}
+
+// dQ for 128 queries of one head (4 waves x 32 queries): loops over the key
+// tiles up to the diagonal, recomputes S^T and dP^T with keys as MFMA rows (a
+// lane owns one query, as in the forward), forms dS^T in registers and
+// accumulates dQ^T += K^T dS^T; K is staged row-major (for S^T) and transposed
+// (for dQ^T), V row-major (for dP^T).
+template <int D>
+__global__ __launch_bounds__(256, 1) void attn_bwd_dq_kernel(AttnShape sh, const bf16_t* __restrict__ qkv,
+                                                              const bf16_t* __restrict__ dout,
+                                                              const float* __restrict__ lse,
+                                                              const float* __restrict__ Dv, bf16_t* __restrict__ dqkv,
+                                                              const float* __restrict__ rope_cs, float scale,
+                                                              float sl2) {
+  constexpr int KP = D + 8, TP = FWD_BKV + 8;
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[FWD_BKV * KP];
+  __shared__ __attribute__((aligned(16))) bf16_t Vs[FWD_BKV * KP];
+  __shared__ __attribute__((aligned(16))) bf16_t Kt[D * TP];
+
+  const int S = sh.seq, nq = sh.nq, nkv = sh.nkv;
+  const int nqt = (S + FWD_BQ - 1) / FWD_BQ;
+  const int qt = nqt - 1 - (int)blockIdx.x;  // longest rows first
+  const int h = blockIdx.y, b = blockIdx.z, kvh = h / (nq / nkv);
+  const int64_t ld = (int64_t)(nq + 2 * nkv) * D;
+  const int64_t ldo = (int64_t)nq * D;
+  const bf16_t* base = qkv + (int64_t)b * S * ld;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, lr = lane & 31, lh = lane >> 5;
+  const int q0 = qt * FWD_BQ;
+  const int qrow = q0 + 32 * wave + lr;
+  const int wave_qmin = q0 + 32 * wave, wave_qmax = wave_qmin + 31;
+  const bool qok = qrow < S;
+
+  u32x4 qf[D / 16], df[D / 16];
+#pragma unroll
+  for (int s = 0; s < D / 16; ++s) {
+    qf[s] = qok ? load16(base + (int64_t)qrow * ld + h * D + 16 * s + 8 * lh) : u32x4{0u, 0u, 0u, 0u};
+    df[s] = qok ? load16(dout + ((int64_t)b * S + qrow) * ldo + h * D + 16 * s + 8 * lh) : u32x4{0u, 0u, 0u, 0u};
+  }
+  const float lse2 = qok ? lse[((int64_t)b * nq + h) * S + qrow] * LOG2E : 0.f;
+  const float Dq = qok ? Dv[((int64_t)b * nq + h) * S + qrow] : 0.f;
+
+  f32x16 dq[D / 32];
 #pragma unroll
   for (int i = 0; i < D / 32; ++i)
 #pragma unroll
-    for (int rq = 0; rq < 4; ++rq) {
-      const int d = 32 * i + 8 * rq + 4 * lh;
-      float kv4[4], vv4[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        vv4[e] = dv[i][4 * rq + e];
-        const float x1 = dk[i][4 * rq + e] * scale;
-        if (rope_cs == nullptr) {
-          kv4[e] = x1;
-        } else if (i < IP) {
-          const float x2 = dk[(i + IP) % (D / 32)][4 * rq + e] * scale;
-          const float c = rope_cs[(int64_t)kvrow * HALF + d + e];
-          const float sn = rope_cs[(int64_t)S * HALF + (int64_t)kvrow * HALF + d + e];
-          kv4[e] = x1 * c + x2 * sn;
-        } else {
-          const float x0 = dk[(i - IP + D / 32) % (D / 32)][4 * rq + e] * scale;
-          const int dl = d - HALF + e;
-          const float c = rope_cs[(int64_t)kvrow * HALF + dl];
-          const float sn = rope_cs[(int64_t)S * HALF + (int64_t)kvrow * HALF + dl];
-          kv4[e] = x1 * c - x0 * sn;
-        }
-      }
-      *(u32x2*)(krow + d) = u32x2{pack_bf2(kv4[0], kv4[1]), pack_bf2(kv4[2], kv4[3])};
-      *(u32x2*)(vrow + d) = u32x2{pack_bf2(vv4[0], vv4[1]), pack_bf2(vv4[2], vv4[3])};
-    }
-}
+    for (int r = 0; r < 16; ++r) dq[i][r] = 0.f;
 
-// dq (bf16, into the q columns of dqkv) = scale * dq_acc, un-rotated.
-template <int D>
-__global__ __launch_bounds__(256) void attn_bwd_post_kernel(AttnShape sh, const float* __restrict__ dq_acc,
-                                                            bf16_t* __restrict__ dqkv, const float* __restrict__ rope_cs,
-                                                            float scale) {
-  constexpr int HALF = D / 2, QPH = HALF / 4;  // quads of pair-columns per head
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t total = (int64_t)sh.batch * sh.seq * sh.nq * QPH;
-  if (idx >= total) return;
-  const int qd = (int)(idx % QPH);
-  const int64_t th = idx / QPH;  // token * nq + head
-  const int h = (int)(th % sh.nq);
-  const int64_t t = th / sh.nq;
-  const int pos = (int)(t % sh.seq);
-  const float* src = dq_acc + th * D + 4 * qd;
-  const f32x4 a = *(const f32x4*)src, c2 = *(const f32x4*)(src + HALF);
-  float lo[4], hi[4];
+  const int kv_end = min(S, q0 + FWD_BQ);
+  const int nkt = (kv_end + FWD_BKV - 1) / FWD_BKV;
+  for (int kt = 0; kt < nkt; ++kt) {
+    const int kv0 = kt * FWD_BKV;
+    __syncthreads();
+    stage_rows<FWD_BKV, D, KP, 256>(Ks, base, ld, kv0, S, (nq + kvh) * D, tid);
+    stage_rows<FWD_BKV, D, KP, 256>(Vs, base, ld, kv0, S, (nq + nkv + kvh) * D, tid);
+    stage_transposed<FWD_BKV, D, TP, 256>(Kt, base, ld, kv0, S, (nq + kvh) * D, tid);
+    __syncthreads();
+    if (kv0 > wave_qmax) continue;
+
+    f32x16 sacc[FWD_BKV / 32], pacc[FWD_BKV / 32];
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const float x1 = a[e] * scale, x2 = c2[e] * scale;
-    if (rope_cs) {
-      const int i = 4 * qd + e;
-      const float c = rope_cs[(int64_t)pos * HALF + i], s = rope_cs[(int64_t)sh.seq * HALF + (int64_t)pos * HALF + i];
-      lo[e] = x1 * c + x2 * s;
-      hi[e] = x2 * c - x1 * s;
-    } else {
-      lo[e] = x1;
-      hi[e] = x2;
+    for (int bb = 0; bb < FWD_BKV / 32; ++bb) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sacc[bb][r] = pacc[bb][r] = 0.f;
+#pragma unroll
+      for (int s = 0; s < D / 16; ++s) {
+        sacc[bb] = mfma32(load16(&Ks[(32 * bb + lr) * KP + 16 * s + 8 * lh]), qf[s], sacc[bb]);
+        pacc[bb] = mfma32(load16(&Vs[(32 * bb + lr) * KP + 16 * s + 8 * lh]), df[s], pacc[bb]);
+      }
+    }
+    // lane holds query qrow, keys kv0 + 32bb + 8(r/4) + 4lh + r%4
+#pragma unroll
+    for (int bb = 0; bb < FWD_BKV / 32; ++bb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int kv = kv0 + 32 * bb + 8 * (r >> 2) + 4 * lh + (r & 3);
+        const float p = (kv <= qrow && kv < S) ? exp2f(sacc[bb][r] * sl2 - lse2) : 0.f;
+        pacc[bb][r] = p * (pacc[bb][r] - Dq);
+      }
+#pragma unroll
+    for (int s = 0; s < FWD_BKV / 16; ++s) {
+      const u32x4 sf = pack_frag(pacc[s >> 1], 8 * (s & 1));
+#pragma unroll
+      for (int i = 0; i < D / 32; ++i)
+        dq[i] = mfma32(ld_pair8(&Kt[(32 * i + lr) * TP + 16 * s + 4 * lh]), sf, dq[i]);
     }
   }
-  const int64_t ld = (int64_t)(sh.nq + 2 * sh.nkv) * D;
-  bf16_t* dst = dqkv + t * ld + h * D + 4 * qd;
-  *(u32x2*)dst = u32x2{pack_bf2(lo[0], lo[1]), pack_bf2(lo[2], lo[3])};
-  *(u32x2*)(dst + HALF) = u32x2{pack_bf2(hi[0], hi[1]), pack_bf2(hi[2], hi[3])};
+  if (!qok) return;
+  unrotate_store<D>(dq, scale, rope_cs, S, qrow, lh, dqkv + ((int64_t)b * S + qrow) * ld + h * D);
 }
 
 template <int D>
@@ -437,19 +455,18 @@ hipError_t attn_bwd_t(const AttnShape& sh, const bf16_t* qkv, const bf16_t* o, c
                       bf16_t* dqkv, const float* rope_cs, void* ws, hipStream_t s) {
   const int64_t T = (int64_t)sh.batch * sh.seq;
   float* Dv = (float*)ws;
-  float* dq_acc = Dv + ((T * sh.nq + 63) / 64) * 64;
-  hipLaunchKernelGGL((attn_bwd_pre_kernel<D>), dim3((unsigned)((T + 3) / 4)), dim3(256), 0, s, sh, o, dout, Dv, dq_acc);
+  hipLaunchKernelGGL((attn_bwd_pre_kernel<D>), dim3((unsigned)((T + 3) / 4)), dim3(256), 0, s, sh, o, dout, Dv);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const float scale = 1.0f / sqrtf((float)D);
-  const dim3 grid((sh.seq + BWD_BKV - 1) / BWD_BKV, sh.nkv, sh.batch);
-  hipLaunchKernelGGL((attn_bwd_kernel<D>), grid, dim3(256), 0, s, sh, qkv, dout, lse, (const float*)Dv, dq_acc, dqkv,
+  const dim3 gkv((sh.seq + BWD_BKV - 1) / BWD_BKV, sh.nkv, sh.batch);
+  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D>), gkv, dim3(256), 0, s, sh, qkv, dout, lse, (const float*)Dv, dqkv,
                      rope_cs, scale, scale * LOG2E);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int64_t n = T * sh.nq * (D / 8);
-  hipLaunchKernelGGL((attn_bwd_post_kernel<D>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, sh,
-                     (const float*)dq_acc, dqkv, rope_cs, scale);
+  const dim3 gq((sh.seq + FWD_BQ - 1) / FWD_BQ, sh.nq, sh.batch);
+  hipLaunchKernelGGL((attn_bwd_dq_kernel<D>), gq, dim3(256), 0, s, sh, qkv, dout, lse, (const float*)Dv, dqkv,
+                     rope_cs, scale, scale * LOG2E);
   return hipGetLastError();
 }
 
@@ -463,7 +480,7 @@ hipError_t attn_fwd(const AttnShape& sh, const bf16_t* qkv, bf16_t* o, float* ls
 
 size_t attn_bwd_workspace(const AttnShape& sh) {
   const int64_t T = (int64_t)sh.batch * sh.seq;
-  return (size_t)(((T * sh.nq + 63) / 64) * 64 + T * sh.nq * sh.d) * sizeof(float);
+  return (size_t)(T * sh.nq) * sizeof(float);
 }
 
 hipError_t attn_bwd(const AttnShape& sh, const bf16_t* qkv, const bf16_t* o, const float* lse, const bf16_t* dout,

@@ -1,16 +1,23 @@
 // bf16 matrix products on gfx950 matrix cores (v_mfma_f32_32x32x16_bf16) with
 // fp32 accumulation and fused epilogues for the decoder block.
 //
-// One workgroup computes a BM x BN tile of C; its waves split the tile into
-// WM x WN wave tiles of 32x32 MFMA blocks.  Operand tiles of 64 k-values are
-// staged global -> registers -> LDS, double-buffered in LDS, so the global
-// loads of tile k+1 are in flight while the matrix cores work on tile k.
-// LDS always holds both operands k-contiguous ([row][k], rows padded by 8
-// elements so the 16-byte fragment reads of 32 consecutive rows hit distinct
-// banks).  An operand that is k-strided in memory (the weight-gradient and
-// input-gradient products) is loaded as 8x8 blocks with coalesced 16-byte
-// row loads and transposed in registers before its LDS store, so the matrix
-// core loop is identical for every layout.
+// One workgroup of 4 waves computes a 256x256 tile of C; each wave owns a
+// 128x128 quarter (16 MFMA blocks of 32x32, accumulators in AGPRs).  Operand
+// tiles of 64 k-values move global -> registers -> LDS with buffer loads that
+// return zero outside the operand, so ragged edges need no branches.  Two LDS
+// stages: the loads of tile k+1 are in flight while the matrix cores consume
+// tile k, and are stored to the other stage afterwards.
+//
+// LDS layouts (no padding; an XOR swizzle of the 16-byte chunk index keeps
+// the fragment reads free of bank conflicts):
+//   k-contiguous operand  [256 rows][64 k]  128-byte rows, chunk c of row r at
+//                         slot c ^ ((r/2) % 8); fragments are 16-byte reads.
+//   k-strided operand     [64 k][256 cols]  512-byte rows, chunk c of row k at
+//                         slot c ^ 4(k % 4); fragments are two transposing
+//                         8-byte reads (ds_read_b64_tr_b16), which hand each
+//                         lane 4 consecutive k of one column.
+// So every layout (forward, input-gradient and weight-gradient products)
+// runs the same matrix-core loop without any explicit transpose.
 //
 // Each MFMA takes the B fragment as its first operand and the A fragment as
 // its second, so that a lane ends up holding four consecutive output columns
@@ -19,14 +26,23 @@
 #include "common.h"
 #include "kernels.h"
 
+#define LDS_AS __attribute__((address_space(3)))
+
 namespace ls {
 
 namespace {
 
-constexpr int KT = 64;           // k extent of a staged tile
-constexpr int PITCH = KT + 8;    // LDS row pitch in bf16 elements (144 bytes)
-constexpr int GROUP_M = 8;       // tile rows per group in the launch order
-constexpr int EPI_ROPE64 = 100;  // EPI_ROPE for 64-wide heads
+constexpr int BM = 256, BN = 256, KT = 64;  // tile
+constexpr int WGM = 2, WGN = 2;             // waves
+constexpr int NT = 64 * WGM * WGN;
+constexpr int WM = BM / WGM, WN = BN / WGN;
+constexpr int TM = WM / 32, TN = WN / 32;
+constexpr int TILE_BYTES = 256 * KT * 2;    // one operand tile in LDS (32 KB)
+constexpr int GROUP_M = 8;                  // tile rows per group in the launch order
+constexpr int EPI_ROPE64 = 100;             // EPI_ROPE for 64-wide heads
+constexpr uint32_t OOB = 0x80000000u;       // a buffer offset past any operand: loads zero
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
 
 // Launch order: workgroups are handed to the 8 XCDs round-robin, so first
 // renumber them so that each XCD receives a contiguous range of logical tiles,
@@ -45,29 +61,152 @@ LS_DEV void map_tile(int wg, int tiles_m, int tiles_n, int& tm, int& tn) {
   tn = in_g / gm;
 }
 
-LS_DEV const bf16_t* seg_row(const GemmArgs& p, int row) {
-  const int s = row >= p.b_start[2] ? 2 : (row >= p.b_start[1] ? 1 : 0);
-  return p.B[s] + (int64_t)(row - p.b_start[s]) * p.ldb;
+// Buffer resource over [base, base + bytes).  Every caller passes wave-uniform
+// values; reading them through readfirstlane lets the compiler keep the
+// resource in scalar registers.
+LS_DEV __amdgpu_buffer_rsrc_t rsrc(const void* base, uint32_t bytes) {
+  const uint64_t a = (uint64_t)base;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+  const uint32_t n = __builtin_amdgcn_readfirstlane(bytes);
+  return __builtin_amdgcn_make_buffer_rsrc((void*)(((uint64_t)hi << 32) | lo), (short)0, (int)n, 0x00020000);
 }
 
-LS_DEV float silu_f(float g) { return g / (1.0f + __expf(-g)); }
+LS_DEV uint32_t clamp_bytes(int64_t b) { return b <= 0 ? 0u : (b >= 0x7fffffff ? 0x7fffffffu : (uint32_t)b); }
 
-template <int BM, int BN, int WGM, int WGN, bool AK, bool BKC, int EPI>
-__global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_kernel(GemmArgs p) {
-  constexpr int NT = 64 * WGM * WGN;
-  constexpr int WM = BM / WGM, WN = BN / WGN;
-  constexpr int TM = WM / 32, TN = WN / 32;
-  // per-thread staged 16-byte pieces of each operand tile
-  constexpr int A_PIECES = BM * KT / 8 / NT;
-  constexpr int B_PIECES = BN * KT / 8 / NT;
-  static_assert(A_PIECES * NT * 8 == BM * KT && B_PIECES * NT * 8 == BN * KT, "tile/threads");
-  static_assert(AK || A_PIECES % 8 == 0, "transposed loads move 8x8 blocks");
-  static_assert(BKC || B_PIECES % 8 == 0, "transposed loads move 8x8 blocks");
+// 16 bytes per lane from a buffer (zero outside it).
+LS_DEV u32x4 load16(__amdgpu_buffer_rsrc_t r, uint32_t voff) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, 0, 0));
+}
 
-  __shared__ __attribute__((aligned(16))) bf16_t As[2][BM * PITCH];
-  __shared__ __attribute__((aligned(16))) bf16_t Bs[2][BN * PITCH];
+// LDS swizzles (XOR on the 16-byte chunk index).  The LDS serves 16 lanes of a
+// 16-byte read (32 lanes of an 8-byte read) per clock across 64 banks, so:
+//  - k-contiguous tiles (128-byte rows): the 16 rows a 16-lane group reads at
+//    one logical chunk must land on 16 distinct 16-byte bank groups of a
+//    256-byte window; row parity picks the half, (r/2) % 8 the slot.
+//  - k-strided tiles (512-byte rows): a 32-lane transposing read covers 4
+//    rows x 64 bytes; XOR with 4 * (k % 4) puts the 4 rows' 64-byte runs on
+//    distinct quarters of a 256-byte window.
+LS_DEV int kc_swz(int r) { return (r >> 1) & 7; }
+LS_DEV int ks_swz(int k) { return 4 * (k & 3); }
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+LS_DEV float silu_f(float g) { return g * __frcp_rn(1.0f + __expf(-g)); }
+
+// One operand: up to three row segments (rows of B may come from three weight
+// matrices).  For a k-contiguous operand the segments split its m/n rows; for a
+// k-strided one they split its k rows.  Segment starts are multiples of 8, so
+// one load instruction (8 rows, or 2 k-rows) never straddles a segment, and the
+// segment, hence the buffer resource, is uniform per instruction.
+// glu (k-contiguous B only): virtual row n is row (n/128)*64 + n%64 of segment
+// (n/64)%2 (gate and up rows interleaved in blocks of 64).
+struct Segs {
+  const bf16_t *b0, *b1, *b2;
+  int s1, s2;  // starts of segments 1 and 2
+  int rows;    // total rows
+  int64_t ld;  // leading dimension in elements
+};
+
+// Resource and first-row index of the segment that holds row `rb` (uniform).
+LS_DEV __amdgpu_buffer_rsrc_t seg_rsrc(const Segs& g, int rb, int& seg_start) {
+  const bf16_t* base;
+  int s0, s_end;
+  if (rb >= g.s2) {
+    base = g.b2; s0 = g.s2; s_end = g.rows;
+  } else if (rb >= g.s1) {
+    base = g.b1; s0 = g.s1; s_end = min(g.s2, g.rows);
+  } else {
+    base = g.b0; s0 = 0; s_end = min(g.s1, g.rows);
+  }
+  seg_start = s0;
+  return rsrc(base, clamp_bytes((int64_t)(s_end - s0) * g.ld * 2));
+}
+
+// Load one 64-k tile of a k-contiguous operand (rows row0 .. row0+255, k0 ..
+// k0+63) into registers: piece jj of lane l is LDS slot l of the 1 KB block j =
+// wave + 4jj, i.e. slot l%8 of row 8j + l/8, holding that row's logical chunk
+// (l%8) ^ kc_swz(row).
+template <bool GLU>
+LS_DEV void load_kc(const Segs& g, const bf16_t* gate, const bf16_t* up, int glu_rows, int row0, int k0, int K,
+                    u32x4* reg, int wave, int lane) {
+#pragma unroll
+  for (int jj = 0; jj < 256 / 8 / 4; ++jj) {
+    const int j = wave + 4 * jj;
+    const int c = (lane & 7) ^ kc_swz(8 * j + (lane >> 3));
+    const int k = k0 + 8 * c;
+    const bool kok = k < K;
+    const int rb = row0 + 8 * j;  // first row of the instruction (uniform)
+    int lrow0;
+    __amdgpu_buffer_rsrc_t r;
+    if constexpr (GLU) {
+      r = rsrc((rb >> 6) & 1 ? up : gate, clamp_bytes((int64_t)glu_rows * g.ld * 2));
+      lrow0 = (rb >> 7) * 64 + (rb & 63);
+    } else {
+      int s0;
+      r = seg_rsrc(g, rb, s0);
+      lrow0 = rb - s0;
+    }
+    const int lrow = lrow0 + (lane >> 3);
+    const uint32_t voff = kok ? (uint32_t)(lrow * g.ld * 2 + k * 2) : OOB;
+    reg[jj] = load16(r, voff);
+  }
+}
+
+// Load one 64-k tile of a k-strided operand (k rows k0 .. k0+63, columns col0 ..
+// col0+255 of `cols`) into registers: piece jj of lane l is LDS slot l of block
+// j = wave + 4jj, i.e. slot l%32 of k-row 2j + l/32, holding that row's logical
+// chunk (l%32) ^ ks_swz(k-row).
+LS_DEV void load_ks(const Segs& g, int col0, int cols, int k0, int K, u32x4* reg, int wave, int lane) {
+  const int lh = lane >> 5;
+#pragma unroll
+  for (int jj = 0; jj < KT / 2 / 4; ++jj) {
+    const int j = wave + 4 * jj;
+    const int kb = k0 + 2 * j;  // first k row of the instruction (uniform)
+    int s0;
+    const __amdgpu_buffer_rsrc_t r = seg_rsrc(g, kb, s0);
+    const int c = (lane & 31) ^ ks_swz(2 * j + lh);
+    const int col = col0 + 8 * c;
+    const int lk = kb - s0 + lh;
+    const uint32_t voff = (kb + lh < K && col < cols) ? (uint32_t)(lk * g.ld * 2 + col * 2) : OOB;
+    reg[jj] = load16(r, voff);
+  }
+}
+
+// Store the pieces of one operand tile: piece jj of lane l goes to LDS slot l of
+// the 1 KB block wave + 4jj.
+LS_DEV void store_tile(const u32x4* reg, bf16_t* lds, int wave, int lane) {
+#pragma unroll
+  for (int jj = 0; jj < 8; ++jj) *(u32x4*)(lds + (wave + 4 * jj) * 512 + lane * 8) = reg[jj];
+}
+
+// Fragment of a k-contiguous tile: lane gets row `r` (tile-local), k = 16s + 8*(lane/32) .. +7.
+LS_DEV u32x4 frag_kc(const bf16_t* lds, int r, int s, int lh) {
+  return *(const u32x4*)(lds + r * KT + 8 * ((2 * s + lh) ^ kc_swz(r)));
+}
+
+// Fragment of a k-strided tile for the 32 columns starting at c32 (tile-local):
+// lane gets column c32 + lane%32, k = 16s + 8*(lane/32) .. +7, via two transposing reads.
+LS_DEV u32x4 frag_ks(const bf16_t* lds, int c32, int s, int lane) {
+  const int g = lane >> 4, q = lane & 15;
+  const int col = c32 + 16 * (g & 1) + 4 * (q & 3);
+  u32x4 out;
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const int kk = 16 * s + 8 * (g >> 1) + 4 * t + (q >> 2);
+    const bf16_t* p = lds + kk * 256 + 8 * ((col >> 3) ^ ks_swz(kk)) + (col & 7);
+    const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS s16x4*)p);
+    const u32x2 w = __builtin_bit_cast(u32x2, v);
+    out[2 * t] = w[0];
+    out[2 * t + 1] = w[1];
+  }
+  return out;
+}
+
+template <bool AK, bool BKC, int EPI>
+__global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
+  __shared__ __attribute__((aligned(1024))) bf16_t lds[2][2][256 * KT];  // [stage][A/B]
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = wave / WGN, wn = wave % WGN;
   const int tiles_m = (p.M + BM - 1) / BM, tiles_n = (p.N + BN - 1) / BN;
   int tm, tn;
@@ -76,110 +215,32 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_kernel(GemmArgs p) {
   const int K = p.K;
   const int nk = (K + KT - 1) / KT;
 
-  // ---- operand sources (fixed for the whole k loop) ------------------------
-  // k-contiguous operand: piece c covers row c/8, k-chunk c%8 of the tile.
-  // k-strided operand: thread owns 8x8 blocks; block b covers k-rows
-  // 8*(b / (R/8)) .. +7 and columns 8*(b % (R/8)) .. +7 of the tile.
-  const bf16_t* a_src[AK ? A_PIECES : A_PIECES / 8];
-  const bf16_t* b_src[BKC ? B_PIECES : 1];
-  if constexpr (AK) {
-#pragma unroll
-    for (int i = 0; i < A_PIECES; ++i) {
-      const int c = tid + i * NT, row = m0 + (c >> 3);
-      a_src[i] = row < p.M ? p.A + (int64_t)row * p.lda + (c & 7) * 8 : nullptr;
-    }
-  } else {
-#pragma unroll
-    for (int i = 0; i < A_PIECES / 8; ++i) {
-      const int b = tid + i * NT, col = m0 + (b % (BM / 8)) * 8;
-      a_src[i] = col < p.M ? p.A + col : nullptr;
-    }
-  }
-  if constexpr (BKC) {
-#pragma unroll
-    for (int i = 0; i < B_PIECES; ++i) {
-      const int c = tid + i * NT, n = n0 + (c >> 3);
-      const bf16_t* src = nullptr;
-      if (p.glu) {
-        const int blk = n >> 6, row = (blk >> 1) * 64 + (n & 63);
-        if (row < p.glu_rows) src = p.B[blk & 1] + (int64_t)row * p.ldb;
-      } else if (n < p.N) {
-        src = seg_row(p, n);
-      }
-      b_src[i] = src ? src + (c & 7) * 8 : nullptr;
-    }
-  }
+  Segs ga, gb;
+  ga.b0 = ga.b1 = ga.b2 = p.A;
+  ga.s1 = ga.s2 = 1 << 30;
+  ga.rows = AK ? p.M : K;
+  ga.ld = p.lda;
+  gb.b0 = p.B[0];
+  gb.b1 = p.B[1] ? p.B[1] : p.B[0];
+  gb.b2 = p.B[2] ? p.B[2] : p.B[0];
+  gb.s1 = p.b_start[1];
+  gb.s2 = p.b_start[2];
+  gb.rows = BKC ? p.N : K;
+  gb.ld = p.ldb;
 
-  u32x4 ra[A_PIECES], rb[B_PIECES];
-  const u32x4 zero4 = {0u, 0u, 0u, 0u};
-
+  const bf16_t* gate = p.B[0];
+  const bf16_t* up = p.B[1];
+  u32x4 ra[8], rb[8];  // one tile of each operand in flight: global -> registers -> LDS
   auto load_tiles = [&](int kt) {
     const int k0 = kt * KT;
-    if constexpr (AK) {
-#pragma unroll
-      for (int i = 0; i < A_PIECES; ++i) {
-        const int c = tid + i * NT, k = k0 + (c & 7) * 8;
-        ra[i] = (a_src[i] && k < K) ? *(const u32x4*)(a_src[i] + k0) : zero4;
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < A_PIECES / 8; ++i) {
-        const int b = tid + i * NT, kr = k0 + (b / (BM / 8)) * 8;
-#pragma unroll
-        for (int j = 0; j < 8; ++j)
-          ra[i * 8 + j] = (a_src[i] && kr + j < K) ? *(const u32x4*)(a_src[i] + (int64_t)(kr + j) * p.lda) : zero4;
-      }
-    }
-    if constexpr (BKC) {
-#pragma unroll
-      for (int i = 0; i < B_PIECES; ++i) {
-        const int c = tid + i * NT, k = k0 + (c & 7) * 8;
-        rb[i] = (b_src[i] && k < K) ? *(const u32x4*)(b_src[i] + k0) : zero4;
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < B_PIECES / 8; ++i) {
-        const int b = tid + i * NT, kr = k0 + (b / (BN / 8)) * 8, col = n0 + (b % (BN / 8)) * 8;
-#pragma unroll
-        for (int j = 0; j < 8; ++j)
-          rb[i * 8 + j] = (col < p.N && kr + j < K) ? *(const u32x4*)(seg_row(p, kr + j) + col) : zero4;
-      }
-    }
+    if constexpr (AK) load_kc<false>(ga, nullptr, nullptr, 0, m0, k0, K, ra, wave, lane);
+    else load_ks(ga, m0, p.M, k0, K, ra, wave, lane);
+    if constexpr (BKC) load_kc<EPI == EPI_GLU_FWD>(gb, gate, up, p.glu_rows, n0, k0, K, rb, wave, lane);
+    else load_ks(gb, n0, p.N, k0, K, rb, wave, lane);
   };
-
-  auto store_tiles = [&](int buf) {
-    if constexpr (AK) {
-#pragma unroll
-      for (int i = 0; i < A_PIECES; ++i) {
-        const int c = tid + i * NT;
-        *(u32x4*)&As[buf][(c >> 3) * PITCH + (c & 7) * 8] = ra[i];
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < A_PIECES / 8; ++i) {
-        const int b = tid + i * NT, kb = b / (BM / 8), mb = b % (BM / 8);
-        u32x4 t[8];
-        transpose8x8(&ra[i * 8], t);
-#pragma unroll
-        for (int c = 0; c < 8; ++c) *(u32x4*)&As[buf][(mb * 8 + c) * PITCH + kb * 8] = t[c];
-      }
-    }
-    if constexpr (BKC) {
-#pragma unroll
-      for (int i = 0; i < B_PIECES; ++i) {
-        const int c = tid + i * NT;
-        *(u32x4*)&Bs[buf][(c >> 3) * PITCH + (c & 7) * 8] = rb[i];
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < B_PIECES / 8; ++i) {
-        const int b = tid + i * NT, kb = b / (BN / 8), nb = b % (BN / 8);
-        u32x4 t[8];
-        transpose8x8(&rb[i * 8], t);
-#pragma unroll
-        for (int c = 0; c < 8; ++c) *(u32x4*)&Bs[buf][(nb * 8 + c) * PITCH + kb * 8] = t[c];
-      }
-    }
+  auto store_tiles = [&](int stage) {
+    store_tile(ra, lds[stage][0], wave, lane);
+    store_tile(rb, lds[stage][1], wave, lane);
   };
 
   f32x16 acc[TM][TN];
@@ -191,155 +252,259 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_kernel(GemmArgs p) {
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
   const int lr = lane & 31, lh = lane >> 5;
-  const int a_row0 = wm * WM + lr, b_row0 = wn * WN + lr;
+
+  // Fragments of step s+1 are read while the matrix cores work on step s; the
+  // scheduling barriers keep the compiler from sinking the reads to their use.
+  auto compute = [&](int stage) {
+    const bf16_t* as = lds[stage][0];
+    const bf16_t* bs = lds[stage][1];
+    u32x4 af[2][TM], bfr[2][TN];
+    auto load_frags = [&](int s, int buf) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+        af[buf][i] = AK ? frag_kc(as, wm * WM + 32 * i + lr, s, lh) : frag_ks(as, wm * WM + 32 * i, s, lane);
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        bfr[buf][j] = BKC ? frag_kc(bs, wn * WN + 32 * j + lr, s, lh) : frag_ks(bs, wn * WN + 32 * j, s, lane);
+    };
+    load_frags(0, 0);
+#pragma unroll
+    for (int s = 0; s < KT / 16; ++s) {
+      if (s + 1 < KT / 16) load_frags(s + 1, (s + 1) & 1);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32(bfr[s & 1][j], af[s & 1][i], acc[i][j]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
 
   load_tiles(0);
   store_tiles(0);
   __syncthreads();
   for (int kt = 0; kt < nk; ++kt) {
     const int cur = kt & 1;
-    if (kt + 1 < nk) load_tiles(kt + 1);
-    const bf16_t* as = As[cur];
-    const bf16_t* bs = Bs[cur];
-#pragma unroll
-    for (int s = 0; s < KT / 16; ++s) {
-      u32x4 af[TM], bfr[TN];
-#pragma unroll
-      for (int i = 0; i < TM; ++i) af[i] = *(const u32x4*)&as[(a_row0 + 32 * i) * PITCH + 16 * s + 8 * lh];
-#pragma unroll
-      for (int j = 0; j < TN; ++j) bfr[j] = *(const u32x4*)&bs[(b_row0 + 32 * j) * PITCH + 16 * s + 8 * lh];
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32(bfr[j], af[i], acc[i][j]);
-    }
+    if (kt + 1 < nk) load_tiles(kt + 1);  // in flight during the matrix-core work below
+    compute(cur);
     if (kt + 1 < nk) store_tiles(cur ^ 1);
     __syncthreads();
   }
 
-  // ---- epilogue: lane holds C[m][n .. n+3], m = row of the lane, n = 8q + 4*lh
-  const int wn0 = n0 + wn * WN;
+  // ---- epilogue ---------------------------------------------------------------
+  // Lane holds C[32i + lr][32j + 8q + 4lh .. +3] of its wave tile (acc[i][j][4q..]).
+  // Results go through a 32 KB LDS region per wave so that global loads and
+  // stores move whole 256-byte row segments (16 bytes per lane).  Staging rows
+  // are unpadded (bf16: 128 rows x 256 B, fp32: 64 rows x 512 B) with the
+  // 16-byte chunk index XOR-swizzled by the row, so the column-wise writes
+  // from the MFMA layout and the row-wise reads both avoid bank conflicts.
+  bf16_t* stg = &lds[0][0][0] + wave * 16384;
+  float* stgf = (float*)stg;
+  auto sb = [](int r, int col) { return r * 128 + ((((col >> 3) ^ (r & 15)) << 3) | (col & 7)); };
+  auto sf = [](int r, int col) { return r * 128 + ((((col >> 2) ^ (r & 31)) << 2) | (col & 3)); };
+  const int mw = m0 + wm * WM, nw = n0 + wn * WN;
+
+  // bf16 staging: 128 rows x 128 columns -> rows of `dst` (row-major, ld), at columns col(cc)
+  auto put4 = [&](int r, int c, const float v[4]) {
+    *(u32x2*)&stg[sb(r, c)] = u32x2{pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3])};
+  };
+  auto flush_bf16 = [&](bf16_t* dst, int64_t ldd, int col0, int ncols_valid) {
+#pragma unroll 4
+    for (int t = 0; t < 32; ++t) {
+      const int c = lane + 64 * t, r = c >> 4, cc = c & 15;
+      const u32x4 v = *(const u32x4*)&stg[sb(r, cc * 8)];
+      if (mw + r < p.M && cc * 8 < ncols_valid) *(u32x4*)(dst + (int64_t)(mw + r) * ldd + col0 + cc * 8) = v;
+    }
+  };
+
+  if constexpr (EPI == EPI_F32 || EPI == EPI_RESID) {
+    // fp32 staging in two halves of 64 rows; the residual / old gradient is read coalesced.
 #pragma unroll
-  for (int i = 0; i < TM; ++i) {
-    const int m = m0 + wm * WM + 32 * i + lr;
-    if (m >= p.M) continue;
-    if constexpr (EPI == EPI_GLU_FWD) {
-      static_assert(WN == 128, "gate/up interleave needs 128-column wave tiles");
+    for (int half = 0; half < 2; ++half) {
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+      for (int ii = 0; ii < 2; ++ii)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int col = wn0 / 2 + 32 * j + 8 * q + 4 * lh;
-          if (col >= p.glu_I) continue;
-          float g[4], u[4];
-          uint32_t pg[2], pu[2], pa[2];
+        for (int j = 0; j < TN; ++j)
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            g[e] = acc[i][j][4 * q + e];
-            u[e] = acc[i][j + 2][4 * q + e];
+          for (int q = 0; q < 4; ++q) {
+            const f32x4 v = {acc[2 * half + ii][j][4 * q], acc[2 * half + ii][j][4 * q + 1],
+                             acc[2 * half + ii][j][4 * q + 2], acc[2 * half + ii][j][4 * q + 3]};
+            *(f32x4*)&stgf[sf(32 * ii + lr, 32 * j + 8 * q + 4 * lh)] = v;
           }
-#pragma unroll
-          for (int e = 0; e < 2; ++e) {
-            pg[e] = pack_bf2(g[2 * e], g[2 * e + 1]);
-            pu[e] = pack_bf2(u[2 * e], u[2 * e + 1]);
-            pa[e] = pack_bf2(silu_f(g[2 * e]) * u[2 * e], silu_f(g[2 * e + 1]) * u[2 * e + 1]);
+#pragma unroll 4
+      for (int t = 0; t < 32; ++t) {
+        const int c = lane + 64 * t, r = c >> 5, cc = c & 31;
+        f32x4 v = *(const f32x4*)&stgf[sf(r, cc * 4)];
+        const int m = mw + 64 * half + r, n = nw + cc * 4;
+        if (m < p.M && n < p.N) {
+          if constexpr (EPI == EPI_F32) {
+            const int sg = m >= p.f_start[2] ? 2 : (m >= p.f_start[1] ? 1 : 0);
+            float* base = sg == 2 ? p.F[2] : (sg == 1 ? p.F[1] : p.F[0]);
+            const int fs = sg == 2 ? p.f_start[2] : (sg == 1 ? p.f_start[1] : 0);
+            float* dst = base + (int64_t)(m - fs) * p.ldf + n;
+            if (p.accumulate) v += *(const f32x4*)dst;
+            *(f32x4*)dst = v;
+          } else {
+            const u32x2 rw = *(const u32x2*)(p.R + (int64_t)m * p.ldc + n);
+            v[0] += bf_lo(rw[0]);
+            v[1] += bf_hi(rw[0]);
+            v[2] += bf_lo(rw[1]);
+            v[3] += bf_hi(rw[1]);
+            *(u32x2*)(p.C + (int64_t)m * p.ldc + n) = u32x2{pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3])};
           }
-          bf16_t* row = p.C + (int64_t)m * p.ldc;
-          *(u32x2*)(row + col) = u32x2{pg[0], pg[1]};
-          *(u32x2*)(row + p.glu_I + col) = u32x2{pu[0], pu[1]};
-          *(u32x2*)(p.act + (int64_t)m * p.glu_I + col) = u32x2{pa[0], pa[1]};
-        }
-    } else if constexpr (EPI == EPI_ROPE || EPI == EPI_ROPE64) {
-      constexpr int HD = EPI == EPI_ROPE ? 128 : 64, HALF = HD / 2, JP = HALF / 32;
-      static_assert(WN % HD == 0, "wave tiles hold whole heads");
-      const int pos = m % p.seq;
-      const float* cs = p.rope_cs + (int64_t)pos * HALF;
-      const float* sn = p.rope_cs + (int64_t)p.seq * HALF + (int64_t)pos * HALF;
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int nb = wn0 + 32 * j;
-        if (nb >= p.N) continue;
-        const bool rot = nb < p.rope_cols;
-        const int dcol = (32 * j) % HD;  // wave tiles start on a head boundary
-        if (rot && dcol >= HALF) continue;  // written together with its partner
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int n = nb + 8 * q + 4 * lh;
-          bf16_t* out = p.C + (int64_t)m * p.ldc + n;
-          if (!rot || j + JP >= TN) {
-            *(u32x2*)out = u32x2{pack_bf2(acc[i][j][4 * q], acc[i][j][4 * q + 1]),
-                                 pack_bf2(acc[i][j][4 * q + 2], acc[i][j][4 * q + 3])};
-            continue;
-          }
-          float lo[4], hi[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int dc = dcol + 8 * q + 4 * lh + e;
-            const float c = cs[dc], s = sn[dc];
-            const float x1 = acc[i][j][4 * q + e], x2 = acc[i][(j + JP) % TN][4 * q + e];
-            lo[e] = x1 * c - x2 * s;
-            hi[e] = x2 * c + x1 * s;
-          }
-          *(u32x2*)out = u32x2{pack_bf2(lo[0], lo[1]), pack_bf2(lo[2], lo[3])};
-          *(u32x2*)(out + HALF) = u32x2{pack_bf2(hi[0], hi[1]), pack_bf2(hi[2], hi[3])};
         }
       }
-    } else {
+    }
+  } else if constexpr (EPI == EPI_GLU_FWD) {
+    static_assert(WN == 128, "gate/up interleave needs 128-column wave tiles");
+    // subtiles j = 0, 1 hold gate columns, j = 2, 3 the up columns of the same 64 features
+    const int col0 = nw / 2;  // first feature of the wave tile
+    const int nvalid = p.glu_I - col0;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
       for (int j = 0; j < TN; ++j)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          const int n = wn0 + 32 * j + 8 * q + 4 * lh;
-          if (n >= p.N) continue;
           float v[4];
 #pragma unroll
           for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * q + e];
-          if constexpr (EPI == EPI_F32) {
-            const int s = m >= p.f_start[2] ? 2 : (m >= p.f_start[1] ? 1 : 0);
-            float* dst = p.F[s] + (int64_t)(m - p.f_start[s]) * p.ldf + n;
-            f32x4 o = {v[0], v[1], v[2], v[3]};
-            if (p.accumulate) o += *(const f32x4*)dst;
-            *(f32x4*)dst = o;
-          } else if constexpr (EPI == EPI_GLU_BWD) {
-            const bf16_t* gsrc = p.gu_in + (int64_t)m * 2 * p.glu_I + n;
-            const u32x2 gw = *(const u32x2*)gsrc;
-            const u32x2 uw = *(const u32x2*)(gsrc + p.glu_I);
-            const float g[4] = {bf_lo(gw[0]), bf_hi(gw[0]), bf_lo(gw[1]), bf_hi(gw[1])};
-            const float u[4] = {bf_lo(uw[0]), bf_hi(uw[0]), bf_lo(uw[1]), bf_hi(uw[1])};
-            float dg[4], du[4];
+          put4(32 * i + lr, 32 * j + 8 * q + 4 * lh, v);  // [g(64) | u(64)] per row
+        }
+#pragma unroll 4
+    for (int t = 0; t < 32; ++t) {
+      const int c = lane + 64 * t, r = c >> 4, cc = c & 15;
+      const u32x4 v = *(const u32x4*)&stg[sb(r, cc * 8)];
+      const int f = (cc & 7) * 8;  // feature offset within the 64
+      if (mw + r < p.M && f < nvalid)
+        *(u32x4*)(p.C + (int64_t)(mw + r) * p.ldc + (cc < 8 ? 0 : p.glu_I) + col0 + f) = v;
+    }
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          float v[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float g = acc[i][j][4 * q + e], u = acc[i][j + 2][4 * q + e];
+            v[e] = silu_f(g) * u;
+          }
+          put4(32 * i + lr, 32 * j + 8 * q + 4 * lh, v);
+        }
+#pragma unroll 4
+    for (int t = 0; t < 16; ++t) {
+      const int c = lane + 64 * t, r = c >> 3, cc = c & 7;
+      const u32x4 v = *(const u32x4*)&stg[sb(r, cc * 8)];
+      if (mw + r < p.M && cc * 8 < nvalid) *(u32x4*)(p.act + (int64_t)(mw + r) * p.glu_I + col0 + cc * 8) = v;
+    }
+  } else if constexpr (EPI == EPI_GLU_BWD) {
+    // acc = dact.  Per 32-row block: the saved gate and up values are read
+    // coalesced into LDS, dg = dact u silu'(g) and du = dact silu(g) replace
+    // them in place, and both go out coalesced.
+    bf16_t* sg_ = stg;             // gate / dg rows (32 x 128)
+    bf16_t* su_ = stg + 32 * 128;  // up / du rows
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const int mb = mw + 32 * i;
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const int c = lane + 64 * t, r = c >> 4, cc = c & 15;
+        u32x4 gv = {0u, 0u, 0u, 0u}, uv = {0u, 0u, 0u, 0u};
+        if (mb + r < p.M && nw + cc * 8 < p.N) {
+          const bf16_t* src = p.gu_in + (int64_t)(mb + r) * 2 * p.glu_I + nw + cc * 8;
+          gv = *(const u32x4*)src;
+          uv = *(const u32x4*)(src + p.glu_I);
+        }
+        *(u32x4*)&sg_[sb(r, cc * 8)] = gv;
+        *(u32x4*)&su_[sb(r, cc * 8)] = uv;
+      }
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int off = sb(lr, 32 * j + 8 * q + 4 * lh);
+          const u32x2 gw = *(const u32x2*)&sg_[off], uw = *(const u32x2*)&su_[off];
+          const float g[4] = {bf_lo(gw[0]), bf_hi(gw[0]), bf_lo(gw[1]), bf_hi(gw[1])};
+          const float u[4] = {bf_lo(uw[0]), bf_hi(uw[0]), bf_lo(uw[1]), bf_hi(uw[1])};
+          float dg[4], du[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float da = acc[i][j][4 * q + e];
+            const float sgm = __frcp_rn(1.0f + __expf(-g[e]));
+            dg[e] = da * u[e] * sgm * (1.0f + g[e] * (1.0f - sgm));
+            du[e] = da * g[e] * sgm;
+          }
+          *(u32x2*)&sg_[off] = u32x2{pack_bf2(dg[0], dg[1]), pack_bf2(dg[2], dg[3])};
+          *(u32x2*)&su_[off] = u32x2{pack_bf2(du[0], du[1]), pack_bf2(du[2], du[3])};
+        }
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const int c = lane + 64 * t, r = c >> 4, cc = c & 15;
+        if (mb + r < p.M && nw + cc * 8 < p.N) {
+          bf16_t* dst = p.C + (int64_t)(mb + r) * p.ldc + nw + cc * 8;
+          *(u32x4*)dst = *(const u32x4*)&sg_[sb(r, cc * 8)];
+          *(u32x4*)(dst + p.glu_I) = *(const u32x4*)&su_[sb(r, cc * 8)];
+        }
+      }
+    }
+  } else {
+    // EPI_BF16, EPI_ROPE, EPI_ROPE64
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const int m = mw + 32 * i + lr;
+      if constexpr (EPI == EPI_ROPE || EPI == EPI_ROPE64) {
+        constexpr int HD = EPI == EPI_ROPE ? 128 : 64, HALF = HD / 2, JP = HALF / 32;
+        static_assert(WN % HD == 0, "wave tiles hold whole heads");
+        const int pos = (m < p.M ? m : 0) % p.seq;
+        const float* cs = p.rope_cs + (int64_t)pos * HALF;
+        const float* sn = p.rope_cs + (int64_t)p.seq * HALF + (int64_t)pos * HALF;
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const bool rot = nw + 32 * j < p.rope_cols;
+          const int dcol = (32 * j) % HD;  // wave tiles start on a head boundary
+          if (rot && dcol >= HALF) continue;  // written together with its partner
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            float lo[4], hi[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-              const float sg = 1.0f / (1.0f + __expf(-g[e]));
-              du[e] = v[e] * g[e] * sg;
-              dg[e] = v[e] * u[e] * sg * (1.0f + g[e] * (1.0f - sg));
+              const float x1 = acc[i][j][4 * q + e];
+              if (rot && j + JP < TN) {
+                const int dc = dcol + 8 * q + 4 * lh + e;
+                const float c = cs[dc], sv = sn[dc];
+                const float x2 = acc[i][(j + JP) % TN][4 * q + e];
+                lo[e] = x1 * c - x2 * sv;
+                hi[e] = x2 * c + x1 * sv;
+              } else {
+                lo[e] = x1;
+              }
             }
-            bf16_t* out = p.C + (int64_t)m * p.ldc + n;
-            *(u32x2*)out = u32x2{pack_bf2(dg[0], dg[1]), pack_bf2(dg[2], dg[3])};
-            *(u32x2*)(out + p.glu_I) = u32x2{pack_bf2(du[0], du[1]), pack_bf2(du[2], du[3])};
-          } else {
-            bf16_t* out = p.C + (int64_t)m * p.ldc + n;
-            if constexpr (EPI == EPI_RESID) {
-              const u32x2 rw = *(const u32x2*)(p.R + (int64_t)m * p.ldc + n);
-              v[0] += bf_lo(rw[0]);
-              v[1] += bf_hi(rw[0]);
-              v[2] += bf_lo(rw[1]);
-              v[3] += bf_hi(rw[1]);
-            }
-            *(u32x2*)out = u32x2{pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3])};
+            put4(32 * i + lr, 32 * j + 8 * q + 4 * lh, lo);
+            if (rot && j + JP < TN) put4(32 * i + lr, 32 * (j + JP) + 8 * q + 4 * lh, hi);
           }
         }
+      } else {
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            float v[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * q + e];
+            put4(32 * i + lr, 32 * j + 8 * q + 4 * lh, v);
+          }
+      }
     }
+    flush_bf16(p.C, p.ldc, nw, p.N - nw);
   }
 }
 
-// Tile configuration: 256x256 tiles, 4 waves in a 2 x 2 grid (128x128 wave
-// tiles; the gate/up pairing and the RoPE partner columns rely on 128-column
-// wave tiles).
 template <bool AK, bool BKC, int EPI>
 hipError_t launch(const GemmArgs& a, hipStream_t s) {
-  constexpr int BM = 256, BN = 256, WGM = 2, WGN = 2;
   const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_kernel<BM, BN, WGM, WGN, AK, BKC, EPI>), dim3(tiles), dim3(64 * WGM * WGN), 0, s, a);
+  hipLaunchKernelGGL((gemm_kernel<AK, BKC, EPI>), dim3(tiles), dim3(NT), 0, s, a);
   return hipGetLastError();
 }
 
