@@ -24,6 +24,8 @@ METRIC = "decoder-block fwd+bwd TFLOP/s and MFU (bf16), 3B shape seq 2048, 1 MI3
 PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 matrix peak (256 CUs x 4096 FLOP/clk x 2.4 GHz)
 PEAK_HBM_GBS = 8000.0
 DOMINANT = "gate/up projection"  # the largest single kernel launch of the step
+DOMINANT_KERNEL = "gemm_kernel<true, true, 3>"  # its HIP kernel (gate/up product + SwiGLU epilogue)
+COPY_BYTES = 1 << 30  # size of the plain device copy used to calibrate the HBM byte counters
 
 
 def log(*a):
@@ -35,27 +37,57 @@ def dominant_flops(c) -> float:
     return 2.0 * c.tokens * (2 * c.intermediate) * c.hidden
 
 
-def cpu_baseline(c):
-    """The fp64 oracle on a bounded sample: one sequence of the workload."""
+def dominant_traffic():
+    """HBM bytes per launch of the dominant kernel from the committed counter
+    runs, or None when the kernel sources changed since they were taken."""
+    from paper_2510_02483_amd import profiling
+
+    path = profiling.TRAFFIC_JSON
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        entry = json.load(f).get("gate_up_3b")
+    if not entry or entry.get("sources_hash") != profiling.sources_hash():
+        return None
+    return entry["traffic_bytes"]
+
+
+def calibrate_copy(iters: int = 5):
+    """A plain device copy of COPY_BYTES (read once, written once) for the
+    counter calibration run."""
+    import torch
+
+    src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    for _ in range(iters):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": COPY_BYTES, "iters": iters}), flush=True)
+
+
+def cpu_baseline(c, sequences: int):
+    """The fp64 oracle on a bounded sample of the workload: its first
+    `sequences` sequences (the block treats sequences independently)."""
     import numpy as np  # noqa: F401
     from threadpoolctl import threadpool_info
 
     from oracle import block as ob
     from paper_2510_02483_amd import flops, inputs
 
-    one = c.with_(batch=1)
+    n = min(sequences, c.batch)
+    sample = c.with_(batch=n)
     host = inputs.make_inputs(c)
-    f = inputs.to_f64({k: (v[:1] if k in ("x", "dy") else v) for k, v in host.items()})
+    f = inputs.to_f64({k: (v[:n] if k in ("x", "dy") else v) for k, v in host.items()})
     w = {k: f[k] for k in ("wq", "wk", "wv", "wo", "wg", "wu", "wd", "attn_norm", "mlp_norm")}
     t0 = time.perf_counter()
     ob.block_fwd_bwd(f["x"], w, f["dy"], n_q_heads=c.n_q_heads, n_kv_heads=c.n_kv_heads,
                      rope_theta=c.rope_theta, eps=c.rms_eps)
     dt = time.perf_counter() - t0
     threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
-    return {"value": flops.block_fwd_bwd_flops(one) / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads),
+    return {"value": flops.block_fwd_bwd_flops(sample) / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads),
             "kind": "oracle",
-            "sample": f"1 of {c.batch} sequences ({c.seq} tokens) of the same block, fp64 numpy oracle, "
-                      f"{dt:.1f} s wall"}
+            "sample": f"{n} of {c.batch} sequences ({n * c.seq} tokens) of the same block, fp64 numpy oracle "
+                      f"(BLAS matmuls), {dt:.1f} s wall"}
 
 
 def main():
@@ -65,12 +97,19 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="3b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sequences", type=int, default=4, help="sequences in the oracle's timed sample")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="run only a plain 1 GiB device copy (for counter calibration) and exit")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU only: this build runs the block on a single MI355X "
               "(no sharding or collectives); run it with --gpus 1.", file=sys.stderr)
         sys.exit(2)
+
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
 
     import torch
 
@@ -129,14 +168,14 @@ def main():
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(dom_tflops / PEAK_BF16_TFLOPS, 4) if dom_tflops else None,
-            "traffic": None,
+            "traffic": dominant_traffic() if args.config == "3b" else None,
             "launches": n_dom,
             "mean_ms": round(dom_ms, 4),
         },
     }
     if not args.no_cpu_baseline and args.config == "3b":
-        log("timing the fp64 oracle on a one-sequence sample ...")
-        result["cpu_baseline"] = cpu_baseline(c)
+        log("timing the fp64 oracle on a sample of the workload ...")
+        result["cpu_baseline"] = cpu_baseline(c, args.cpu_sequences)
     print(json.dumps(result), flush=True)
 
 
