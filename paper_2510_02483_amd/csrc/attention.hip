@@ -6,25 +6,36 @@
 // v heads of one token in one row), o and dout are [batch*seq, nq*d], lse and
 // D are [batch, nq, seq] fp32.  Query head h reads kv head h / (nq/nkv).
 //
-// Forward (one workgroup = 128 query rows of one head, 4 waves x 32 rows):
-// each wave computes S^T = K Q^T for a 64-key tile with the keys as MFMA rows,
-// so that a lane owns one query (its running max, sum and rescale factor are
-// per-lane scalars; the pair of lanes l, l+32 splits the keys) and the
-// probabilities it holds are already the B operand of O^T += V^T P^T.  V is
-// stored transposed in LDS ([d][key]) so the A operand reads are 8-byte LDS
-// loads in the key order the probabilities arrive in.  The softmax runs in
-// base 2 with the 1/sqrt(d) scale folded into one multiplier.
+// Every streamed operand (K and V tiles in the forward and dQ kernels, Q and
+// dO tiles in the dK/dV kernel) goes from global memory to LDS with buffer
+// loads that write LDS directly, double-buffered: the loads of tile t+1 are in
+// flight while the matrix cores work on tile t, with one barrier per tile.
+// Tiles stay row-major in LDS ([row][d], 16-byte chunks XOR-swizzled by the
+// row).  An operand is read either along d (a 16-byte read per lane: keys or
+// queries as MFMA rows) or transposed (two ds_read_b64_tr_b16 per lane: d as
+// MFMA rows, 4 consecutive keys/queries per read), and the swizzle keeps both
+// kinds of read free of bank conflicts.
 //
+// The probabilities of a 32x32 MFMA block sit in registers with a lane owning
+// one query (forward, dQ) or one key (dK/dV) and holding, for each 16-row
+// k-step, the rows 4lh+{0..3} and 8+4lh+{0..3} (lh = lane/32).  Used as the B
+// operand of the next product they define a permuted k order, and the
+// transposed reads of the A operand fetch their rows in that same order.
+//
+// Forward (one workgroup = 128 queries of one head, 4 waves x 32): S^T = K Q^T
+// per 64-key tile with Q in registers, base-2 online softmax with 1/sqrt(d)
+// folded into one multiplier, O^T += V^T P^T.
 // Backward, two kernels and no atomics.  dK/dV (one workgroup = 128 keys of
-// one kv head, 4 waves x 32 keys): the workgroup loops over the query heads of
-// its group and over 64-row query tiles from the diagonal on; per tile it
-// recomputes S = Q K^T and dP = dO V^T with keys as MFMA columns (a lane owns
-// one key), forms P and dS = P (dP - D) in registers and accumulates
-// dV^T += dO^T P and dK^T += Q^T dS there (the sum over the group's query heads
-// happens in the same registers).  dQ (one workgroup = 128 queries of one
-// head): loops over key tiles like the forward, recomputing S^T and dP^T, and
-// accumulates dQ^T += K^T dS^T.  Both kernels write their gradient already
-// scaled and un-rotated (inverse RoPE) in bf16.
+// one kv head, 4 waves x 32 keys, K and V in registers) loops over the query
+// heads of its group and over 64-query tiles from the diagonal on: S = Q K^T,
+// dP = dO V^T, P and dS = P (dP - D) in registers, dV^T += dO^T P and
+// dK^T += Q^T dS (the sum over the group's heads happens in the same
+// registers).  dQ (one workgroup = 128 queries of one head) loops over key
+// tiles like the forward: S^T, dP^T, dQ^T += K^T dS^T.  Both write their
+// gradient already scaled and un-rotated (inverse RoPE) in bf16.
+//
+// Workgroups are numbered so that the longest (most causal tiles) start
+// first, which balances the triangular work over the compute units.
 #include <math.h>
 
 #include "common.h"
@@ -37,69 +48,121 @@ namespace {
 constexpr float LOG2E = 1.4426950408889634f;
 constexpr float LN2 = 0.6931471805599453f;
 
-constexpr int FWD_BQ = 128, FWD_BKV = 64;
-constexpr int BWD_BKV = 128, BWD_BQ = 64;
+constexpr int BQ = 128;       // queries per workgroup (forward, dQ)
+constexpr int BKV = 64;       // keys per tile (forward, dQ)
+constexpr int BWD_BKV = 128;  // keys per workgroup (dK/dV)
+constexpr int BWD_BQ = 64;    // queries per tile (dK/dV)
 
 LS_DEV u32x4 load16(const bf16_t* p) { return *(const u32x4*)p; }
-LS_DEV u32x4 ld_pair8(const bf16_t* p) {  // elements p[0..3] and p[8..11]
-  const u32x2 lo = *(const u32x2*)p, hi = *(const u32x2*)(p + 8);
-  return u32x4{lo[0], lo[1], hi[0], hi[1]};
-}
 LS_DEV u32x4 pack_frag(const f32x16& v, int r0) {
   return u32x4{pack_bf2(v[r0], v[r0 + 1]), pack_bf2(v[r0 + 2], v[r0 + 3]), pack_bf2(v[r0 + 4], v[r0 + 5]),
                pack_bf2(v[r0 + 6], v[r0 + 7])};
 }
+LS_DEV float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// Stage rows [r0, r0 + ROWS) x columns [col, col + D) of a row-major bf16
-// matrix (leading dimension ld) into LDS transposed: dst[c * PITCH + r] for
-// c < D, r < ROWS.  Rows at or beyond `rows` read as zero.  8x8 blocks,
-// 16-byte loads, register transpose, 16-byte LDS stores.
-template <int ROWS, int D, int PITCH, int NT>
-LS_DEV void stage_transposed(bf16_t* dst, const bf16_t* src, int64_t ld, int r0, int rows, int col, int tid) {
-  constexpr int NB = (ROWS / 8) * (D / 8);
-  for (int b = tid; b < NB; b += NT) {
-    const int rb = b / (D / 8), cb = b % (D / 8);
-    u32x4 in[8], t[8];
+// Row-major LDS tile [rows][D]: 16-byte chunk c of row r sits at slot
+// c ^ tile_swz(r).  The LDS serves 16 lanes of a 16-byte read and 32 lanes of
+// an 8-byte read per clock over 64 banks (a 256-byte window):
+//  - a 16-byte read along d covers 16 consecutive rows at one chunk: the swizzle
+//    is a bijection of r % 16 (D = 128, one row per window) or of (r/2) % 8 for
+//    each parity of r (D = 64, two rows per window);
+//  - a transposing read covers 4 consecutive rows (4-aligned) x 4 consecutive
+//    chunks (4-aligned): the swizzle moves the rows' chunk groups apart
+//    (bits 2..3 of the slot for D = 128, bit 2 plus the window half for D = 64)
+//    while its low two bits only depend on r / 4.
+template <int D>
+LS_DEV int tile_swz(int r) {
+  if constexpr (D == 128) return ((r & 3) << 2) | ((r >> 2) & 3);
+  else return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
+}
+
+// Load rows row0 .. row0+ROWS-1, columns col0 .. col0+D-1 of a row-major bf16
+// matrix (leading dimension ld elements, `rows` rows, covered by the buffer
+// resource r) into an LDS tile; rows at or past `rows` read as zero.  Each
+// instruction fills 1 KB of the tile (64/(D/8) rows); the 4 waves share them.
+template <int D, int ROWS>
+LS_DEV void load_tile(i32x4 r, int64_t ld, int row0, int rows, int col0, bf16_t* t, int wave, int lane) {
+  constexpr int CPR = D / 8, RPI = 64 / CPR, NI = ROWS / RPI;
+  static_assert(NI % 4 == 0, "instructions split evenly over 4 waves");
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int r = r0 + rb * 8 + j;
-      in[j] = r < rows ? load16(src + (int64_t)r * ld + col + cb * 8) : u32x4{0u, 0u, 0u, 0u};
-    }
-    transpose8x8(in, t);
-#pragma unroll
-    for (int c = 0; c < 8; ++c) *(u32x4*)&dst[(cb * 8 + c) * PITCH + rb * 8] = t[c];
+  for (int jj = 0; jj < NI / 4; ++jj) {
+    const int j = wave + 4 * jj;
+    const int rr = j * RPI + lane / CPR;
+    const int c = (lane % CPR) ^ tile_swz<D>(rr);
+    const int gr = row0 + rr;
+    const uint32_t voff = gr < rows ? (uint32_t)(((int64_t)gr * ld + col0 + 8 * c) * 2) : LS_OOB;
+    dma16(r, voff, t + j * 512);
   }
 }
 
-// Stage rows [r0, r0 + ROWS) x columns [col, col + D) row-major: dst[r * PITCH + c].
-template <int ROWS, int D, int PITCH, int NT>
-LS_DEV void stage_rows(bf16_t* dst, const bf16_t* src, int64_t ld, int r0, int rows, int col, int tid) {
-  constexpr int NP = ROWS * D / 8;
-  for (int c = tid; c < NP; c += NT) {
-    const int r = c / (D / 8), ch = c % (D / 8);
-    *(u32x4*)&dst[r * PITCH + ch * 8] =
-        r0 + r < rows ? load16(src + (int64_t)(r0 + r) * ld + col + ch * 8) : u32x4{0u, 0u, 0u, 0u};
+// 64 floats v[i0 .. i0+63] of a buffer of `n` floats (resource r; entries at or
+// past n read as zero) into t[0..63]; t must hold 256 floats (lanes 16..63 of
+// the instruction write zeros to t[64..255]).
+LS_DEV void load_vec64(i32x4 r, int i0, int n, float* t, int lane) {
+  const int i = i0 + 4 * lane;
+  dma16(r, (lane < 16 && i < n) ? (uint32_t)(i * 4) : LS_OOB, t);
+}
+
+// MFMA operand from a tile, read along d: lane gets row `row`, d = 16s + 8lh .. +7.
+template <int D>
+LS_DEV u32x4 row_frag(const bf16_t* t, int row, int s, int lh) {
+  return *(const u32x4*)(t + row * D + 8 * ((2 * s + lh) ^ tile_swz<D>(row)));
+}
+
+// MFMA A operand of the transposed tile: lane gets column (d) c32 + lane%32 and
+// the 8 rows 16s + 4lh + {0..3} and 16s + 8 + 4lh + {0..3} (the permuted k
+// order of probabilities held in registers), via two transposing reads.
+template <int D>
+LS_DEV u32x4 colt_frag(const bf16_t* t, int c32, int s, int lane) {
+  const int g = lane >> 4, q = lane & 15;
+  const int col = c32 + 16 * (g & 1) + 4 * (q & 3);
+  u32x4 out;
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh) {
+    const int kk = 16 * s + 4 * (g >> 1) + 8 * hh + (q >> 2);
+    const bf16_t* p = t + kk * D + 8 * ((col >> 3) ^ tile_swz<D>(kk)) + (col & 7);
+    const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS s16x4*)p);
+    const u32x2 w = __builtin_bit_cast(u32x2, v);
+    out[2 * hh] = w[0];
+    out[2 * hh + 1] = w[1];
   }
+  return out;
+}
+
+// Query-tile workgroups (forward, dQ): the 1-D grid runs the longest tiles
+// (highest query index, most keys) first.
+struct QTile {
+  int qt, h, b;
+};
+LS_DEV QTile q_tile(const AttnShape& sh) {
+  const int nqt = (sh.seq + BQ - 1) / BQ, per = sh.nq * sh.batch;
+  const int x = (int)blockIdx.x;
+  return QTile{nqt - 1 - x / per, (x % per) % sh.nq, (x % per) / sh.nq};
 }
 
 template <int D>
 __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnShape sh, const bf16_t* __restrict__ qkv,
                                                            bf16_t* __restrict__ o, float* __restrict__ lse,
                                                            float sl2) {
-  constexpr int KP = D + 8, VP = FWD_BKV + 8;
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[FWD_BKV * KP];
-  __shared__ __attribute__((aligned(16))) bf16_t Vt[D * VP];
+  __shared__ __attribute__((aligned(1024))) bf16_t Ks[2][BKV * D];
+  __shared__ __attribute__((aligned(1024))) bf16_t Vs[2][BKV * D];
 
   const int S = sh.seq, nq = sh.nq, nkv = sh.nkv;
-  const int nqt = (S + FWD_BQ - 1) / FWD_BQ;
-  const int qt = nqt - 1 - (int)blockIdx.x;  // longest rows first
-  const int h = blockIdx.y, b = blockIdx.z, kvh = h / (nq / nkv);
+  const QTile qtile = q_tile(sh);
+  const int h = qtile.h, b = qtile.b, kvh = h / (nq / nkv);
   const int64_t ld = (int64_t)(nq + 2 * nkv) * D;
   const bf16_t* base = qkv + (int64_t)b * S * ld;
+  const i32x4 rs = rsrc(base, clamp_bytes((int64_t)S * ld * 2));
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, lr = lane & 31, lh = lane >> 5;
-  const int q0 = qt * FWD_BQ;
+  const int q0 = qtile.qt * BQ;
   const int qrow = q0 + 32 * wave + lr;
   const int wave_qmin = q0 + 32 * wave, wave_qmax = wave_qmin + 31;
+  const int kcol = (nq + kvh) * D, vcol = (nq + nkv + kvh) * D;
+
+  const int kv_end = min(S, q0 + BQ);
+  const int nkt = (kv_end + BKV - 1) / BKV;
+  load_tile<D, BKV>(rs, ld, 0, S, kcol, Ks[0], wave, lane);
+  load_tile<D, BKV>(rs, ld, 0, S, vcol, Vs[0], wave, lane);
 
   u32x4 qf[D / 16];
 #pragma unroll
@@ -113,62 +176,64 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnShape sh, const bf
     for (int r = 0; r < 16; ++r) oacc[i][r] = 0.f;
   float m = -INFINITY, l = 0.f;
 
-  const int kv_end = min(S, q0 + FWD_BQ);
-  const int nkt = (kv_end + FWD_BKV - 1) / FWD_BKV;
+  sync_lds();
   for (int kt = 0; kt < nkt; ++kt) {
-    const int kv0 = kt * FWD_BKV;
-    __syncthreads();
-    stage_rows<FWD_BKV, D, KP, 256>(Ks, base, ld, kv0, S, (nq + kvh) * D, tid);
-    stage_transposed<FWD_BKV, D, VP, 256>(Vt, base, ld, kv0, S, (nq + nkv + kvh) * D, tid);
-    __syncthreads();
-    if (kv0 > wave_qmax) continue;  // every key of the tile is in this wave's future
-
-    f32x16 sacc[FWD_BKV / 32];
+    const int cur = kt & 1, kv0 = kt * BKV;
+    if (kt + 1 < nkt) {
+      load_tile<D, BKV>(rs, ld, kv0 + BKV, S, kcol, Ks[cur ^ 1], wave, lane);
+      load_tile<D, BKV>(rs, ld, kv0 + BKV, S, vcol, Vs[cur ^ 1], wave, lane);
+    }
+    if (kv0 <= wave_qmax) {  // else every key of the tile is in this wave's future
+      f32x16 sacc[BKV / 32];
 #pragma unroll
-    for (int bb = 0; bb < FWD_BKV / 32; ++bb) {
+      for (int bb = 0; bb < BKV / 32; ++bb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) sacc[bb][r] = 0.f;
+        for (int r = 0; r < 16; ++r) sacc[bb][r] = 0.f;
 #pragma unroll
       for (int s = 0; s < D / 16; ++s)
-        sacc[bb] = mfma32(load16(&Ks[(32 * bb + lr) * KP + 16 * s + 8 * lh]), qf[s], sacc[bb]);
-    }
-    // lane holds query qrow, keys kv0 + 32bb + 8(r/4) + 4lh + r%4
-    const bool diag = kv0 + FWD_BKV - 1 > wave_qmin;
-    float mx = -INFINITY;
 #pragma unroll
-    for (int bb = 0; bb < FWD_BKV / 32; ++bb)
+        for (int bb = 0; bb < BKV / 32; ++bb)
+          sacc[bb] = mfma32(row_frag<D>(Ks[cur], 32 * bb + lr, s, lh), qf[s], sacc[bb]);
+      // lane holds query qrow, keys kv0 + 32bb + 8(r/4) + 4lh + r%4
+      if (kv0 + BKV - 1 > wave_qmin) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int kv = kv0 + 32 * bb + 8 * (r >> 2) + 4 * lh + (r & 3);
-        float t = sacc[bb][r] * sl2;
-        if (diag && kv > qrow) t = -INFINITY;
-        sacc[bb][r] = t;
-        mx = fmaxf(mx, t);
+        for (int bb = 0; bb < BKV / 32; ++bb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            if (kv0 + 32 * bb + 8 * (r >> 2) + 4 * lh + (r & 3) > qrow) sacc[bb][r] = -INFINITY;
       }
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float mnew = fmaxf(m, mx);
-    const float alpha = exp2f(m - mnew);
-    float ls = 0.f;
+      float mx = -INFINITY;
 #pragma unroll
-    for (int bb = 0; bb < FWD_BKV / 32; ++bb)
+      for (int bb = 0; bb < BKV / 32; ++bb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float p = exp2f(sacc[bb][r] - mnew);
-        sacc[bb][r] = p;
-        ls += p;
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[bb][r]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float mnew = fmaxf(m, mx * sl2);  // key 0 is visible to every query: finite from the first tile on
+      const float alpha = ex2(m - mnew);
+      float ls = 0.f;
+#pragma unroll
+      for (int bb = 0; bb < BKV / 32; ++bb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float p = ex2(fmaf(sacc[bb][r], sl2, -mnew));
+          sacc[bb][r] = p;
+          ls += p;
+        }
+      ls += __shfl_xor(ls, 32);
+      l = l * alpha + ls;
+      m = mnew;
+      if (__builtin_amdgcn_ballot_w64(alpha != 1.0f)) {
+#pragma unroll
+        for (int i = 0; i < D / 32; ++i) oacc[i] *= alpha;
       }
-    ls += __shfl_xor(ls, 32);
-    l = l * alpha + ls;
-    m = mnew;
 #pragma unroll
-    for (int i = 0; i < D / 32; ++i) oacc[i] *= alpha;
+      for (int s = 0; s < BKV / 16; ++s) {
+        const u32x4 pf = pack_frag(sacc[s >> 1], 8 * (s & 1));
 #pragma unroll
-    for (int s = 0; s < FWD_BKV / 16; ++s) {
-      const u32x4 pf = pack_frag(sacc[s >> 1], 8 * (s & 1));
-#pragma unroll
-      for (int i = 0; i < D / 32; ++i)
-        oacc[i] = mfma32(ld_pair8(&Vt[(32 * i + lr) * VP + 16 * s + 4 * lh]), pf, oacc[i]);
+        for (int i = 0; i < D / 32; ++i) oacc[i] = mfma32(colt_frag<D>(Vs[cur], 32 * i, s, lane), pf, oacc[i]);
+      }
     }
+    sync_lds();
   }
 
   if (qrow < S) {
@@ -248,7 +313,8 @@ LS_DEV void unrotate_store(const f32x16 (&acc)[D / 32], float scale, const float
 }
 
 // dK and dV for 128 keys of one kv head (4 waves x 32 keys), summed over the
-// query heads of the group, no atomics.
+// query heads of the group, no atomics.  The 1-D grid runs the key tiles with
+// the most queries after them (lowest key index) first.
 template <int D>
 __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnShape sh, const bf16_t* __restrict__ qkv,
                                                                 const bf16_t* __restrict__ dout,
@@ -256,23 +322,36 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnShape sh, con
                                                                 const float* __restrict__ Dv, bf16_t* __restrict__ dqkv,
                                                                 const float* __restrict__ rope_cs, float scale,
                                                                 float sl2) {
-  constexpr int QP = D + 8, TP = BWD_BQ + 8;
-  __shared__ __attribute__((aligned(16))) bf16_t Qs[BWD_BQ * QP];
-  __shared__ __attribute__((aligned(16))) bf16_t dOs[BWD_BQ * QP];
-  __shared__ __attribute__((aligned(16))) bf16_t Qt[D * TP];
-  __shared__ __attribute__((aligned(16))) bf16_t dOt[D * TP];
-  __shared__ __attribute__((aligned(16))) float lse_s[BWD_BQ];
-  __shared__ __attribute__((aligned(16))) float D_s[BWD_BQ];
+  __shared__ __attribute__((aligned(1024))) bf16_t Qs[2][BWD_BQ * D];
+  __shared__ __attribute__((aligned(1024))) bf16_t dOs[2][BWD_BQ * D];
+  __shared__ __attribute__((aligned(1024))) float Ls[2][256];
+  __shared__ __attribute__((aligned(1024))) float Ds[2][256];
 
   const int S = sh.seq, nq = sh.nq, nkv = sh.nkv, G = nq / nkv;
-  const int kvt = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+  const int per = nkv * sh.batch, x = (int)blockIdx.x;
+  const int kvt = x / per, kvh = (x % per) % nkv, b = (x % per) / nkv;
   const int64_t ld = (int64_t)(nq + 2 * nkv) * D;
   const int64_t ldo = (int64_t)nq * D;
   const bf16_t* base = qkv + (int64_t)b * S * ld;
   const bf16_t* dbase = dout + (int64_t)b * S * ldo;
+  const i32x4 rq_ = rsrc(base, clamp_bytes((int64_t)S * ld * 2));
+  const i32x4 rdo = rsrc(dbase, clamp_bytes((int64_t)S * ldo * 2));
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, lr = lane & 31, lh = lane >> 5;
   const int kv0 = kvt * BWD_BKV;
   const int kvrow = kv0 + 32 * wave + lr;
+
+  // tiles t = 0 .. G*nqt-1: query head kvh*G + t/nqt, queries q_begin + (t%nqt)*BWD_BQ ..
+  const int q_begin = kv0;  // earlier queries see none of these keys
+  const int nqt = (S - q_begin + BWD_BQ - 1) / BWD_BQ;
+  const int ntiles = G * nqt;
+  auto issue = [&](int t, int buf) {
+    const int h = kvh * G + t / nqt, q0 = q_begin + (t % nqt) * BWD_BQ;
+    load_tile<D, BWD_BQ>(rq_, ld, q0, S, h * D, Qs[buf], wave, lane);
+    load_tile<D, BWD_BQ>(rdo, ldo, q0, S, h * D, dOs[buf], wave, lane);
+    if (wave == 0) load_vec64(rsrc(lse + ((int64_t)b * nq + h) * S, (uint32_t)S * 4), q0, S, Ls[buf], lane);
+    if (wave == 1) load_vec64(rsrc(Dv + ((int64_t)b * nq + h) * S, (uint32_t)S * 4), q0, S, Ds[buf], lane);
+  };
+  if (ntiles > 0) issue(0, 0);
 
   u32x4 kf[D / 16], vf[D / 16];
 #pragma unroll
@@ -288,48 +367,38 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnShape sh, con
 #pragma unroll
     for (int r = 0; r < 16; ++r) dk[i][r] = dv[i][r] = 0.f;
 
-  const int q_begin = (kv0 / BWD_BQ) * BWD_BQ;
-  for (int g = 0; g < G; ++g) {
-    const int h = kvh * G + g;
-    const float* lse_h = lse + ((int64_t)b * nq + h) * S;
-    const float* D_h = Dv + ((int64_t)b * nq + h) * S;
-    for (int q0 = q_begin; q0 < S; q0 += BWD_BQ) {
-      __syncthreads();
-      stage_rows<BWD_BQ, D, QP, 256>(Qs, base, ld, q0, S, h * D, tid);
-      stage_rows<BWD_BQ, D, QP, 256>(dOs, dbase, ldo, q0, S, h * D, tid);
-      stage_transposed<BWD_BQ, D, TP, 256>(Qt, base, ld, q0, S, h * D, tid);
-      stage_transposed<BWD_BQ, D, TP, 256>(dOt, dbase, ldo, q0, S, h * D, tid);
-      if (tid < BWD_BQ) {
-        const int q = q0 + tid;
-        lse_s[tid] = q < S ? lse_h[q] * LOG2E : 0.f;
-        D_s[tid] = q < S ? D_h[q] : 0.f;
-      }
-      __syncthreads();
-      if (kv0 + 32 * wave > q0 + BWD_BQ - 1) continue;  // every query of the tile precedes this wave's keys
-
+  sync_lds();
+  for (int t = 0; t < ntiles; ++t) {
+    const int cur = t & 1;
+    const int q0 = q_begin + (t % nqt) * BWD_BQ;
+    if (t + 1 < ntiles) issue(t + 1, cur ^ 1);
+    if (kv0 + 32 * wave <= q0 + BWD_BQ - 1) {  // else every query of the tile precedes this wave's keys
       f32x16 sacc[2], pacc[2];
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
+      for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) sacc[qb][r] = pacc[qb][r] = 0.f;
 #pragma unroll
-        for (int s = 0; s < D / 16; ++s) {
-          sacc[qb] = mfma32(load16(&Qs[(32 * qb + lr) * QP + 16 * s + 8 * lh]), kf[s], sacc[qb]);
-          pacc[qb] = mfma32(load16(&dOs[(32 * qb + lr) * QP + 16 * s + 8 * lh]), vf[s], pacc[qb]);
+      for (int s = 0; s < D / 16; ++s)
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+          sacc[qb] = mfma32(row_frag<D>(Qs[cur], 32 * qb + lr, s, lh), kf[s], sacc[qb]);
+          pacc[qb] = mfma32(row_frag<D>(dOs[cur], 32 * qb + lr, s, lh), vf[s], pacc[qb]);
         }
-      }
       // lane holds key kvrow, queries q0 + 32qb + 8(r/4) + 4lh + r%4
+      const bool edge = q0 < kv0 + BWD_BKV || q0 + BWD_BQ > S;
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
         for (int rq = 0; rq < 4; ++rq) {
           const int ql = 32 * qb + 8 * rq + 4 * lh;
-          const f32x4 L = *(const f32x4*)&lse_s[ql];
-          const f32x4 Dd = *(const f32x4*)&D_s[ql];
+          const f32x4 L = *(const f32x4*)&Ls[cur][ql];
+          const f32x4 Dd = *(const f32x4*)&Ds[cur][ql];
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             const int r = 4 * rq + e, q = q0 + ql + e;
-            const float p = (kvrow <= q && q < S) ? exp2f(sacc[qb][r] * sl2 - L[e]) : 0.f;
+            float p = ex2(fmaf(sacc[qb][r], sl2, -L[e] * LOG2E));
+            if (edge && !(kvrow <= q && q < S)) p = 0.f;
             pacc[qb][r] = p * (pacc[qb][r] - Dd[e]);
             sacc[qb][r] = p;
           }
@@ -340,49 +409,52 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnShape sh, con
         const u32x4 sf = pack_frag(pacc[s >> 1], 8 * (s & 1));
 #pragma unroll
         for (int i = 0; i < D / 32; ++i) {
-          dv[i] = mfma32(ld_pair8(&dOt[(32 * i + lr) * TP + 16 * s + 4 * lh]), pf, dv[i]);
-          dk[i] = mfma32(ld_pair8(&Qt[(32 * i + lr) * TP + 16 * s + 4 * lh]), sf, dk[i]);
+          dv[i] = mfma32(colt_frag<D>(dOs[cur], 32 * i, s, lane), pf, dv[i]);
+          dk[i] = mfma32(colt_frag<D>(Qs[cur], 32 * i, s, lane), sf, dk[i]);
         }
       }
     }
+    sync_lds();
   }
 
   // dK = scale * dS^T Q (un-rotated), dV = P^T dO.  Lane holds key kvrow.
   if (kvrow >= S) return;
-  const int pos = kvrow;
-  unrotate_store<D>(dk, scale, rope_cs, S, pos, lh, dqkv + ((int64_t)b * S + kvrow) * ld + (nq + kvh) * D);
-  unrotate_store<D>(dv, 1.0f, nullptr, S, pos, lh, dqkv + ((int64_t)b * S + kvrow) * ld + (nq + nkv + kvh) * D);
+  unrotate_store<D>(dk, scale, rope_cs, S, kvrow, lh, dqkv + ((int64_t)b * S + kvrow) * ld + (nq + kvh) * D);
+  unrotate_store<D>(dv, 1.0f, nullptr, S, kvrow, lh, dqkv + ((int64_t)b * S + kvrow) * ld + (nq + nkv + kvh) * D);
 }
 
 // dQ for 128 queries of one head (4 waves x 32 queries): loops over the key
 // tiles up to the diagonal, recomputes S^T and dP^T with keys as MFMA rows (a
 // lane owns one query, as in the forward), forms dS^T in registers and
-// accumulates dQ^T += K^T dS^T; K is staged row-major (for S^T) and transposed
-// (for dQ^T), V row-major (for dP^T).
+// accumulates dQ^T += K^T dS^T.
 template <int D>
-__global__ __launch_bounds__(256, 1) void attn_bwd_dq_kernel(AttnShape sh, const bf16_t* __restrict__ qkv,
+__global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(AttnShape sh, const bf16_t* __restrict__ qkv,
                                                               const bf16_t* __restrict__ dout,
                                                               const float* __restrict__ lse,
                                                               const float* __restrict__ Dv, bf16_t* __restrict__ dqkv,
                                                               const float* __restrict__ rope_cs, float scale,
                                                               float sl2) {
-  constexpr int KP = D + 8, TP = FWD_BKV + 8;
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[FWD_BKV * KP];
-  __shared__ __attribute__((aligned(16))) bf16_t Vs[FWD_BKV * KP];
-  __shared__ __attribute__((aligned(16))) bf16_t Kt[D * TP];
+  __shared__ __attribute__((aligned(1024))) bf16_t Ks[2][BKV * D];
+  __shared__ __attribute__((aligned(1024))) bf16_t Vs[2][BKV * D];
 
   const int S = sh.seq, nq = sh.nq, nkv = sh.nkv;
-  const int nqt = (S + FWD_BQ - 1) / FWD_BQ;
-  const int qt = nqt - 1 - (int)blockIdx.x;  // longest rows first
-  const int h = blockIdx.y, b = blockIdx.z, kvh = h / (nq / nkv);
+  const QTile qtile = q_tile(sh);
+  const int h = qtile.h, b = qtile.b, kvh = h / (nq / nkv);
   const int64_t ld = (int64_t)(nq + 2 * nkv) * D;
   const int64_t ldo = (int64_t)nq * D;
   const bf16_t* base = qkv + (int64_t)b * S * ld;
+  const i32x4 rs = rsrc(base, clamp_bytes((int64_t)S * ld * 2));
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, lr = lane & 31, lh = lane >> 5;
-  const int q0 = qt * FWD_BQ;
+  const int q0 = qtile.qt * BQ;
   const int qrow = q0 + 32 * wave + lr;
   const int wave_qmin = q0 + 32 * wave, wave_qmax = wave_qmin + 31;
   const bool qok = qrow < S;
+  const int kcol = (nq + kvh) * D, vcol = (nq + nkv + kvh) * D;
+
+  const int kv_end = min(S, q0 + BQ);
+  const int nkt = (kv_end + BKV - 1) / BKV;
+  load_tile<D, BKV>(rs, ld, 0, S, kcol, Ks[0], wave, lane);
+  load_tile<D, BKV>(rs, ld, 0, S, vcol, Vs[0], wave, lane);
 
   u32x4 qf[D / 16], df[D / 16];
 #pragma unroll
@@ -399,44 +471,45 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dq_kernel(AttnShape sh, const
 #pragma unroll
     for (int r = 0; r < 16; ++r) dq[i][r] = 0.f;
 
-  const int kv_end = min(S, q0 + FWD_BQ);
-  const int nkt = (kv_end + FWD_BKV - 1) / FWD_BKV;
+  sync_lds();
   for (int kt = 0; kt < nkt; ++kt) {
-    const int kv0 = kt * FWD_BKV;
-    __syncthreads();
-    stage_rows<FWD_BKV, D, KP, 256>(Ks, base, ld, kv0, S, (nq + kvh) * D, tid);
-    stage_rows<FWD_BKV, D, KP, 256>(Vs, base, ld, kv0, S, (nq + nkv + kvh) * D, tid);
-    stage_transposed<FWD_BKV, D, TP, 256>(Kt, base, ld, kv0, S, (nq + kvh) * D, tid);
-    __syncthreads();
-    if (kv0 > wave_qmax) continue;
-
-    f32x16 sacc[FWD_BKV / 32], pacc[FWD_BKV / 32];
+    const int cur = kt & 1, kv0 = kt * BKV;
+    if (kt + 1 < nkt) {
+      load_tile<D, BKV>(rs, ld, kv0 + BKV, S, kcol, Ks[cur ^ 1], wave, lane);
+      load_tile<D, BKV>(rs, ld, kv0 + BKV, S, vcol, Vs[cur ^ 1], wave, lane);
+    }
+    if (kv0 <= wave_qmax) {
+      f32x16 sacc[BKV / 32], pacc[BKV / 32];
 #pragma unroll
-    for (int bb = 0; bb < FWD_BKV / 32; ++bb) {
+      for (int bb = 0; bb < BKV / 32; ++bb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) sacc[bb][r] = pacc[bb][r] = 0.f;
+        for (int r = 0; r < 16; ++r) sacc[bb][r] = pacc[bb][r] = 0.f;
 #pragma unroll
-      for (int s = 0; s < D / 16; ++s) {
-        sacc[bb] = mfma32(load16(&Ks[(32 * bb + lr) * KP + 16 * s + 8 * lh]), qf[s], sacc[bb]);
-        pacc[bb] = mfma32(load16(&Vs[(32 * bb + lr) * KP + 16 * s + 8 * lh]), df[s], pacc[bb]);
+      for (int s = 0; s < D / 16; ++s)
+#pragma unroll
+        for (int bb = 0; bb < BKV / 32; ++bb) {
+          sacc[bb] = mfma32(row_frag<D>(Ks[cur], 32 * bb + lr, s, lh), qf[s], sacc[bb]);
+          pacc[bb] = mfma32(row_frag<D>(Vs[cur], 32 * bb + lr, s, lh), df[s], pacc[bb]);
+        }
+      // lane holds query qrow, keys kv0 + 32bb + 8(r/4) + 4lh + r%4
+      const bool diag = kv0 + BKV - 1 > wave_qmin;
+#pragma unroll
+      for (int bb = 0; bb < BKV / 32; ++bb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int kv = kv0 + 32 * bb + 8 * (r >> 2) + 4 * lh + (r & 3);
+          float p = ex2(fmaf(sacc[bb][r], sl2, -lse2));
+          if (diag && kv > qrow) p = 0.f;
+          pacc[bb][r] = p * (pacc[bb][r] - Dq);
+        }
+#pragma unroll
+      for (int s = 0; s < BKV / 16; ++s) {
+        const u32x4 sf = pack_frag(pacc[s >> 1], 8 * (s & 1));
+#pragma unroll
+        for (int i = 0; i < D / 32; ++i) dq[i] = mfma32(colt_frag<D>(Ks[cur], 32 * i, s, lane), sf, dq[i]);
       }
     }
-    // lane holds query qrow, keys kv0 + 32bb + 8(r/4) + 4lh + r%4
-#pragma unroll
-    for (int bb = 0; bb < FWD_BKV / 32; ++bb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int kv = kv0 + 32 * bb + 8 * (r >> 2) + 4 * lh + (r & 3);
-        const float p = (kv <= qrow && kv < S) ? exp2f(sacc[bb][r] * sl2 - lse2) : 0.f;
-        pacc[bb][r] = p * (pacc[bb][r] - Dq);
-      }
-#pragma unroll
-    for (int s = 0; s < FWD_BKV / 16; ++s) {
-      const u32x4 sf = pack_frag(pacc[s >> 1], 8 * (s & 1));
-#pragma unroll
-      for (int i = 0; i < D / 32; ++i)
-        dq[i] = mfma32(ld_pair8(&Kt[(32 * i + lr) * TP + 16 * s + 4 * lh]), sf, dq[i]);
-    }
+    sync_lds();
   }
   if (!qok) return;
   unrotate_store<D>(dq, scale, rope_cs, S, qrow, lh, dqkv + ((int64_t)b * S + qrow) * ld + h * D);
@@ -444,9 +517,9 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dq_kernel(AttnShape sh, const
 
 template <int D>
 hipError_t attn_fwd_t(const AttnShape& sh, const bf16_t* qkv, bf16_t* o, float* lse, hipStream_t s) {
-  const dim3 grid((sh.seq + FWD_BQ - 1) / FWD_BQ, sh.nq, sh.batch);
+  const unsigned grid = (unsigned)((sh.seq + BQ - 1) / BQ) * sh.nq * sh.batch;
   const float sl2 = LOG2E / sqrtf((float)D);
-  hipLaunchKernelGGL((attn_fwd_kernel<D>), grid, dim3(256), 0, s, sh, qkv, o, lse, sl2);
+  hipLaunchKernelGGL((attn_fwd_kernel<D>), dim3(grid), dim3(256), 0, s, sh, qkv, o, lse, sl2);
   return hipGetLastError();
 }
 
@@ -459,13 +532,13 @@ hipError_t attn_bwd_t(const AttnShape& sh, const bf16_t* qkv, const bf16_t* o, c
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const float scale = 1.0f / sqrtf((float)D);
-  const dim3 gkv((sh.seq + BWD_BKV - 1) / BWD_BKV, sh.nkv, sh.batch);
-  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D>), gkv, dim3(256), 0, s, sh, qkv, dout, lse, (const float*)Dv, dqkv,
-                     rope_cs, scale, scale * LOG2E);
+  const unsigned gkv = (unsigned)((sh.seq + BWD_BKV - 1) / BWD_BKV) * sh.nkv * sh.batch;
+  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D>), dim3(gkv), dim3(256), 0, s, sh, qkv, dout, lse, (const float*)Dv,
+                     dqkv, rope_cs, scale, scale * LOG2E);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const dim3 gq((sh.seq + FWD_BQ - 1) / FWD_BQ, sh.nq, sh.batch);
-  hipLaunchKernelGGL((attn_bwd_dq_kernel<D>), gq, dim3(256), 0, s, sh, qkv, dout, lse, (const float*)Dv, dqkv,
+  const unsigned gq = (unsigned)((sh.seq + BQ - 1) / BQ) * sh.nq * sh.batch;
+  hipLaunchKernelGGL((attn_bwd_dq_kernel<D>), dim3(gq), dim3(256), 0, s, sh, qkv, dout, lse, (const float*)Dv, dqkv,
                      rope_cs, scale, scale * LOG2E);
   return hipGetLastError();
 }

@@ -43,6 +43,49 @@ LS_DEV void transpose8x8(const u32x4 in[8], u32x4 out[8]) {
   }
 }
 
+// ---- buffer loads -----------------------------------------------------------
+#define LDS_AS __attribute__((address_space(3)))
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+constexpr uint32_t LS_OOB = 0x80000000u;  // a buffer offset past any operand: loads zero
+
+// Buffer resource over [base, base + bytes) (raw buffer, stride 0).  Every
+// caller passes wave-uniform values; reading them through readfirstlane keeps
+// the resource in scalar registers.
+LS_DEV i32x4 rsrc(const void* base, uint32_t bytes) {
+  const uint64_t a = (uint64_t)base;
+  return i32x4{(int32_t)__builtin_amdgcn_readfirstlane((uint32_t)a),
+               (int32_t)__builtin_amdgcn_readfirstlane((uint32_t)(a >> 32) & 0xffffu),
+               (int32_t)__builtin_amdgcn_readfirstlane(bytes), 0x00020000};
+}
+
+LS_DEV uint32_t clamp_bytes(int64_t b) { return b <= 0 ? 0u : (b >= 0x7fffffff ? 0x7fffffffu : (uint32_t)b); }
+
+// 16 bytes per lane from a buffer (zero outside it) straight into LDS: lane l's
+// bytes land at lds + 16 l (the address is uniform over the wave).  Issued as
+// inline assembly so that the compiler does not see the LDS write: it would
+// otherwise make every later LDS read wait for all loads in flight.  The
+// caller orders the LDS reads with explicit vmcnt waits and barriers.
+LS_DEV void dma16(i32x4 r, uint32_t voff, const void* lds) {
+  const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(const LDS_AS void*)lds);
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "s"(m0), "v"(voff), "s"(r)
+               : "memory", "m0");
+}
+
+// Wait for every buffer->LDS load of this wave and every LDS access, then for
+// the whole workgroup.  A plain s_barrier: __syncthreads() does not know about
+// the inline-assembly loads; the empty asm statements keep the compiler from
+// moving LDS accesses across it.
+LS_DEV void sync_lds() {
+  __builtin_amdgcn_s_waitcnt(0x0070);  // vmcnt(0) lgkmcnt(0)
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 LS_DEV float wave_max(float v) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));

@@ -3,10 +3,15 @@
 //
 // One workgroup of 4 waves computes a 256x256 tile of C; each wave owns a
 // 128x128 quarter (16 MFMA blocks of 32x32, accumulators in AGPRs).  Operand
-// tiles of 64 k-values move global -> registers -> LDS with buffer loads that
-// return zero outside the operand, so ragged edges need no branches.  Two LDS
-// stages: the loads of tile k+1 are in flight while the matrix cores consume
-// tile k, and are stored to the other stage afterwards.
+// tiles of 64 k-values move global -> LDS with buffer loads that write LDS
+// directly (16 bytes per lane, no staging registers) and return zero outside
+// the operand, so ragged edges need no branches.  Two LDS stages of 64 KB:
+// tile k+1 is in flight while the matrix cores consume tile k.
+//
+// The tile depth is set by the load path: a k-contiguous operand row
+// contributes KT*2 bytes per tile, and the buffer->LDS path moves 128-byte row
+// pieces at well over one and a half times the rate of 64-byte ones (each
+// piece is one L1->L2 request and the number of requests in flight is capped).
 //
 // LDS layouts (no padding; an XOR swizzle of the 16-byte chunk index keeps
 // the fragment reads free of bank conflicts):
@@ -26,23 +31,22 @@
 #include "common.h"
 #include "kernels.h"
 
-#define LDS_AS __attribute__((address_space(3)))
 
 namespace ls {
 
 namespace {
 
 constexpr int BM = 256, BN = 256, KT = 64;  // tile
+constexpr int KSTEPS = KT / 16;             // MFMA k-steps per tile
 constexpr int WGM = 2, WGN = 2;             // waves
 constexpr int NT = 64 * WGM * WGN;
 constexpr int WM = BM / WGM, WN = BN / WGN;
 constexpr int TM = WM / 32, TN = WN / 32;
-constexpr int TILE_BYTES = 256 * KT * 2;    // one operand tile in LDS (32 KB)
+constexpr int TILE_ELEMS = 256 * KT;        // one operand tile in LDS (32 KB)
 constexpr int GROUP_M = 8;                  // tile rows per group in the launch order
 constexpr int EPI_ROPE64 = 100;             // EPI_ROPE for 64-wide heads
-constexpr uint32_t OOB = 0x80000000u;       // a buffer offset past any operand: loads zero
+constexpr uint32_t OOB = LS_OOB;
 
-typedef short s16x4 __attribute__((ext_vector_type(4)));
 
 // Launch order: workgroups are handed to the 8 XCDs round-robin, so first
 // renumber them so that each XCD receives a contiguous range of logical tiles,
@@ -61,29 +65,12 @@ LS_DEV void map_tile(int wg, int tiles_m, int tiles_n, int& tm, int& tn) {
   tn = in_g / gm;
 }
 
-// Buffer resource over [base, base + bytes).  Every caller passes wave-uniform
-// values; reading them through readfirstlane lets the compiler keep the
-// resource in scalar registers.
-LS_DEV __amdgpu_buffer_rsrc_t rsrc(const void* base, uint32_t bytes) {
-  const uint64_t a = (uint64_t)base;
-  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
-  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
-  const uint32_t n = __builtin_amdgcn_readfirstlane(bytes);
-  return __builtin_amdgcn_make_buffer_rsrc((void*)(((uint64_t)hi << 32) | lo), (short)0, (int)n, 0x00020000);
-}
-
-LS_DEV uint32_t clamp_bytes(int64_t b) { return b <= 0 ? 0u : (b >= 0x7fffffff ? 0x7fffffffu : (uint32_t)b); }
-
-// 16 bytes per lane from a buffer (zero outside it).
-LS_DEV u32x4 load16(__amdgpu_buffer_rsrc_t r, uint32_t voff) {
-  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, 0, 0));
-}
-
 // LDS swizzles (XOR on the 16-byte chunk index).  The LDS serves 16 lanes of a
 // 16-byte read (32 lanes of an 8-byte read) per clock across 64 banks, so:
-//  - k-contiguous tiles (128-byte rows): the 16 rows a 16-lane group reads at
-//    one logical chunk must land on 16 distinct 16-byte bank groups of a
-//    256-byte window; row parity picks the half, (r/2) % 8 the slot.
+//  - k-contiguous tiles (128-byte rows, 8 chunks): the 16 rows a 16-lane group
+//    reads at one logical chunk must land on 16 distinct 16-byte bank groups of
+//    a 256-byte window; r % 2 picks the row's half of the window, (r/2) % 8
+//    the slot.
 //  - k-strided tiles (512-byte rows): a 32-lane transposing read covers 4
 //    rows x 64 bytes; XOR with 4 * (k % 4) puts the 4 rows' 64-byte runs on
 //    distinct quarters of a 256-byte window.
@@ -107,7 +94,7 @@ struct Segs {
 };
 
 // Resource and first-row index of the segment that holds row `rb` (uniform).
-LS_DEV __amdgpu_buffer_rsrc_t seg_rsrc(const Segs& g, int rb, int& seg_start) {
+LS_DEV i32x4 seg_rsrc(const Segs g, int rb, int& seg_start) {
   const bf16_t* base;
   int s0, s_end;
   if (rb >= g.s2) {
@@ -121,61 +108,50 @@ LS_DEV __amdgpu_buffer_rsrc_t seg_rsrc(const Segs& g, int rb, int& seg_start) {
   return rsrc(base, clamp_bytes((int64_t)(s_end - s0) * g.ld * 2));
 }
 
-// Load one 64-k tile of a k-contiguous operand (rows row0 .. row0+255, k0 ..
-// k0+63) into registers: piece jj of lane l is LDS slot l of the 1 KB block j =
-// wave + 4jj, i.e. slot l%8 of row 8j + l/8, holding that row's logical chunk
-// (l%8) ^ kc_swz(row).
+// One load instruction of a 64-k tile of a k-contiguous operand (rows row0 ..
+// row0+255, k0 .. k0+63); a wave issues jj = 0..7.  Instruction j = wave + 4jj
+// fills the 1 KB block j of the tile, i.e. rows 8j .. 8j+7; lane l writes slot
+// l%8 of row 8j + l/8 with that row's logical chunk (l%8) ^ kc_swz(row), so the
+// 8 lanes of a row fetch its whole 128-byte piece.
 template <bool GLU>
-LS_DEV void load_kc(const Segs& g, const bf16_t* gate, const bf16_t* up, int glu_rows, int row0, int k0, int K,
-                    u32x4* reg, int wave, int lane) {
-#pragma unroll
-  for (int jj = 0; jj < 256 / 8 / 4; ++jj) {
-    const int j = wave + 4 * jj;
-    const int c = (lane & 7) ^ kc_swz(8 * j + (lane >> 3));
-    const int k = k0 + 8 * c;
-    const bool kok = k < K;
-    const int rb = row0 + 8 * j;  // first row of the instruction (uniform)
-    int lrow0;
-    __amdgpu_buffer_rsrc_t r;
-    if constexpr (GLU) {
-      r = rsrc((rb >> 6) & 1 ? up : gate, clamp_bytes((int64_t)glu_rows * g.ld * 2));
-      lrow0 = (rb >> 7) * 64 + (rb & 63);
-    } else {
-      int s0;
-      r = seg_rsrc(g, rb, s0);
-      lrow0 = rb - s0;
-    }
-    const int lrow = lrow0 + (lane >> 3);
-    const uint32_t voff = kok ? (uint32_t)(lrow * g.ld * 2 + k * 2) : OOB;
-    reg[jj] = load16(r, voff);
-  }
-}
-
-// Load one 64-k tile of a k-strided operand (k rows k0 .. k0+63, columns col0 ..
-// col0+255 of `cols`) into registers: piece jj of lane l is LDS slot l of block
-// j = wave + 4jj, i.e. slot l%32 of k-row 2j + l/32, holding that row's logical
-// chunk (l%32) ^ ks_swz(k-row).
-LS_DEV void load_ks(const Segs& g, int col0, int cols, int k0, int K, u32x4* reg, int wave, int lane) {
-  const int lh = lane >> 5;
-#pragma unroll
-  for (int jj = 0; jj < KT / 2 / 4; ++jj) {
-    const int j = wave + 4 * jj;
-    const int kb = k0 + 2 * j;  // first k row of the instruction (uniform)
+LS_DEV void dma_kc(const Segs g, const bf16_t* gate, const bf16_t* up, int glu_rows, int row0, int k0, int K,
+                   bf16_t* lds, int wave, int lane, int jj) {
+  const int j = wave + 4 * jj;
+  const int rr = 8 * j + (lane >> 3);
+  const int c = (lane & 7) ^ kc_swz(rr);
+  const int k = k0 + 8 * c;
+  const int rb = row0 + 8 * j;  // first row of the instruction (uniform)
+  int lrow0;
+  i32x4 r;
+  if constexpr (GLU) {
+    r = rsrc((rb >> 6) & 1 ? up : gate, clamp_bytes((int64_t)glu_rows * g.ld * 2));
+    lrow0 = (rb >> 7) * 64 + (rb & 63);
+  } else {
     int s0;
-    const __amdgpu_buffer_rsrc_t r = seg_rsrc(g, kb, s0);
-    const int c = (lane & 31) ^ ks_swz(2 * j + lh);
-    const int col = col0 + 8 * c;
-    const int lk = kb - s0 + lh;
-    const uint32_t voff = (kb + lh < K && col < cols) ? (uint32_t)(lk * g.ld * 2 + col * 2) : OOB;
-    reg[jj] = load16(r, voff);
+    r = seg_rsrc(g, rb, s0);
+    lrow0 = rb - s0;
   }
+  const int lrow = lrow0 + (lane >> 3);
+  const uint32_t voff = k < K ? (uint32_t)(lrow * g.ld * 2 + k * 2) : OOB;
+  dma16(r, voff, lds + j * 512);
 }
 
-// Store the pieces of one operand tile: piece jj of lane l goes to LDS slot l of
-// the 1 KB block wave + 4jj.
-LS_DEV void store_tile(const u32x4* reg, bf16_t* lds, int wave, int lane) {
-#pragma unroll
-  for (int jj = 0; jj < 8; ++jj) *(u32x4*)(lds + (wave + 4 * jj) * 512 + lane * 8) = reg[jj];
+// One load instruction of a 64-k tile of a k-strided operand (k rows k0 ..
+// k0+63, columns col0 .. col0+255 of `cols`); a wave issues jj = 0..7.
+// Instruction j = wave + 4jj fills k-rows 2j and 2j+1; lane l writes slot l%32
+// of k-row 2j + l/32 with that row's logical chunk (l%32) ^ ks_swz(k-row).
+// Segment starts are even.
+LS_DEV void dma_ks(const Segs g, int col0, int cols, int k0, int K, bf16_t* lds, int wave, int lane, int jj) {
+  const int lh = lane >> 5;
+  const int j = wave + 4 * jj;
+  const int kb = k0 + 2 * j;  // first k row of the instruction (uniform)
+  int s0;
+  const i32x4 r = seg_rsrc(g, kb, s0);
+  const int c = (lane & 31) ^ ks_swz(2 * j + lh);
+  const int col = col0 + 8 * c;
+  const int lk = kb - s0 + lh;
+  const uint32_t voff = (kb + lh < K && col < cols) ? (uint32_t)(lk * g.ld * 2 + col * 2) : OOB;
+  dma16(r, voff, lds + j * 512);
 }
 
 // Fragment of a k-contiguous tile: lane gets row `r` (tile-local), k = 16s + 8*(lane/32) .. +7.
@@ -203,7 +179,9 @@ LS_DEV u32x4 frag_ks(const bf16_t* lds, int c32, int s, int lane) {
 
 template <bool AK, bool BKC, int EPI>
 __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
-  __shared__ __attribute__((aligned(1024))) bf16_t lds[2][2][256 * KT];  // [stage][A/B]
+  // Two LDS stages of [A tile | B tile].  The buffer->LDS loads are inline
+  // assembly the compiler does not see, so the stage can be picked at run time.
+  __shared__ __attribute__((aligned(1024))) bf16_t lds[2][2 * TILE_ELEMS];
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -230,17 +208,16 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
 
   const bf16_t* gate = p.B[0];
   const bf16_t* up = p.B[1];
-  u32x4 ra[8], rb[8];  // one tile of each operand in flight: global -> registers -> LDS
-  auto load_tiles = [&](int kt) {
+  // Load instruction q (0..15) of tile kt into stage st: q < 8 are the A tile's, the rest B's.
+  auto issue = [&](int kt, bf16_t* st, int q) {
     const int k0 = kt * KT;
-    if constexpr (AK) load_kc<false>(ga, nullptr, nullptr, 0, m0, k0, K, ra, wave, lane);
-    else load_ks(ga, m0, p.M, k0, K, ra, wave, lane);
-    if constexpr (BKC) load_kc<EPI == EPI_GLU_FWD>(gb, gate, up, p.glu_rows, n0, k0, K, rb, wave, lane);
-    else load_ks(gb, n0, p.N, k0, K, rb, wave, lane);
-  };
-  auto store_tiles = [&](int stage) {
-    store_tile(ra, lds[stage][0], wave, lane);
-    store_tile(rb, lds[stage][1], wave, lane);
+    if (q < 8) {
+      if constexpr (AK) dma_kc<false>(ga, nullptr, nullptr, 0, m0, k0, K, st, wave, lane, q);
+      else dma_ks(ga, m0, p.M, k0, K, st, wave, lane, q);
+    } else {
+      if constexpr (BKC) dma_kc<EPI == EPI_GLU_FWD>(gb, gate, up, p.glu_rows, n0, k0, K, st + TILE_ELEMS, wave, lane, q - 8);
+      else dma_ks(gb, n0, p.N, k0, K, st + TILE_ELEMS, wave, lane, q - 8);
+    }
   };
 
   f32x16 acc[TM][TN];
@@ -253,43 +230,58 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
 
   const int lr = lane & 31, lh = lane >> 5;
 
-  // Fragments of step s+1 are read while the matrix cores work on step s; the
-  // scheduling barriers keep the compiler from sinking the reads to their use.
-  auto compute = [&](int stage) {
-    const bf16_t* as = lds[stage][0];
-    const bf16_t* bs = lds[stage][1];
-    u32x4 af[2][TM], bfr[2][TN];
-    auto load_frags = [&](int s, int buf) {
+  // The k loop is one continuous stream of 16-k steps (four per 64-k tile):
+  // while the matrix cores work on one step, the fragments of the next step
+  // are read from LDS, across tile boundaries too.  At the start of tile kk
+  // the other stage (tile kk-1) is free, and the loads of tile kk+1 go there;
+  // before the last step of tile kk every wave waits for its own loads of tile
+  // kk+1 (vmcnt) and then for the other waves (barrier), and only then reads
+  // the first fragments of tile kk+1.  The same barrier tells every wave that
+  // all reads of tile kk are done before tile kk+2 overwrites its stage.
+  u32x4 af[2][TM], bfr[2][TN];
+  auto load_frags = [&](int stage, int s, int buf) {
+    const bf16_t* as = lds[stage];
+    const bf16_t* bs = lds[stage] + TILE_ELEMS;
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
-        af[buf][i] = AK ? frag_kc(as, wm * WM + 32 * i + lr, s, lh) : frag_ks(as, wm * WM + 32 * i, s, lane);
+    for (int i = 0; i < TM; ++i)
+      af[buf][i] = AK ? frag_kc(as, wm * WM + 32 * i + lr, s, lh) : frag_ks(as, wm * WM + 32 * i, s, lane);
 #pragma unroll
-      for (int j = 0; j < TN; ++j)
-        bfr[buf][j] = BKC ? frag_kc(bs, wn * WN + 32 * j + lr, s, lh) : frag_ks(bs, wn * WN + 32 * j, s, lane);
-    };
-    load_frags(0, 0);
-#pragma unroll
-    for (int s = 0; s < KT / 16; ++s) {
-      if (s + 1 < KT / 16) load_frags(s + 1, (s + 1) & 1);
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32(bfr[s & 1][j], af[s & 1][i], acc[i][j]);
-      __builtin_amdgcn_sched_barrier(0);
-    }
+    for (int j = 0; j < TN; ++j)
+      bfr[buf][j] = BKC ? frag_kc(bs, wn * WN + 32 * j + lr, s, lh) : frag_ks(bs, wn * WN + 32 * j, s, lane);
   };
+  auto mfmas = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) acc[i][j] = mfma32(bfr[buf][j], af[buf][i], acc[i][j]);
+  };
+  auto sync_tile = []() { sync_lds(); };
 
-  load_tiles(0);
-  store_tiles(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) load_tiles(kt + 1);  // in flight during the matrix-core work below
-    compute(cur);
-    if (kt + 1 < nk) store_tiles(cur ^ 1);
-    __syncthreads();
+#pragma unroll
+  for (int q = 0; q < 16; ++q) issue(0, lds[0], q);
+  sync_tile();
+  load_frags(0, 0, 0);
+  for (int kk = 0; kk < nk; ++kk) {
+    const int cur = kk & 1;
+    if (kk + 1 < nk) {
+#pragma unroll
+      for (int q = 0; q < 16; ++q) issue(kk + 1, lds[cur ^ 1], q);
+    }
+#pragma unroll
+    for (int s = 0; s < KSTEPS; ++s) {
+      const int buf = s & 1;
+      __builtin_amdgcn_sched_barrier(0);
+      if (s + 1 < KSTEPS) {
+        load_frags(cur, s + 1, buf ^ 1);
+      } else if (kk + 1 < nk) {
+        sync_tile();
+        load_frags(cur ^ 1, 0, buf ^ 1);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      mfmas(buf);
+    }
   }
+  sync_tile();  // every wave is done with both stages before they become staging space
 
   // ---- epilogue ---------------------------------------------------------------
   // Lane holds C[32i + lr][32j + 8q + 4lh .. +3] of its wave tile (acc[i][j][4q..]).
@@ -298,7 +290,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
   // are unpadded (bf16: 128 rows x 256 B, fp32: 64 rows x 512 B) with the
   // 16-byte chunk index XOR-swizzled by the row, so the column-wise writes
   // from the MFMA layout and the row-wise reads both avoid bank conflicts.
-  bf16_t* stg = &lds[0][0][0] + wave * 16384;
+  bf16_t* stg = &lds[wave >> 1][(wave & 1) * TILE_ELEMS];  // 32 KB per wave
   float* stgf = (float*)stg;
   auto sb = [](int r, int col) { return r * 128 + ((((col >> 3) ^ (r & 15)) << 3) | (col & 7)); };
   auto sf = [](int r, int col) { return r * 128 + ((((col >> 2) ^ (r & 31)) << 2) | (col & 3)); };
