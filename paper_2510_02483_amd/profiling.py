@@ -113,7 +113,7 @@ def main():
     t.add_argument("--write", required=True)
     t.add_argument("--copy-fetch", required=True)
     t.add_argument("--copy-write", required=True)
-    t.add_argument("--copy-kernel", default="elementwise")
+    t.add_argument("--copy-kernel", default="copyBuffer")
     t.add_argument("--copy-bytes", type=float, required=True)
     t.add_argument("--out", required=True)
     t.add_argument("--cmd", required=True)
