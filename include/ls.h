@@ -190,6 +190,16 @@ int ls_gemm_nn(int64_t M, int64_t N, int64_t K, const ls_bf16* A, const ls_bf16*
 int ls_gemm_tn(int64_t M, int64_t N, int64_t K, const ls_bf16* A, const ls_bf16* B,
                float* C, int accumulate, void* stream);
 
+/* Tile shape of the matrix products (tuning and testing).  By default every
+ * product launch picks its workgroup tile (256 or 192 rows x 256 or 192
+ * columns, where its epilogue allows) to minimise waves of workgroups times
+ * tile area on the device's compute units.  ls_gemm_tile_override(bm, bn)
+ * forces bm x bn (each 256 or 192) for every later launch in the process that
+ * allows it (others keep 256 x 256); (0, 0) restores the automatic choice.
+ * Process-wide setting, not tied to a stream.  Returns LS_ERR_SHAPE for
+ * other sizes. */
+int ls_gemm_tile_override(int32_t bm, int32_t bn);
+
 /* ---- kernel timing (diagnostics) --------------------------------------------
  * Measures one named kernel launch of the calls above with HIP events on the
  * stream it runs on.  ls_timing_begin arms recording for launches whose label

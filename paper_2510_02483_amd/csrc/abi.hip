@@ -860,6 +860,11 @@ int ls_gemm_nn(int64_t M, int64_t N, int64_t K, const ls_bf16* A, const ls_bf16*
   return LS_OK;
 }
 
+int ls_gemm_tile_override(int32_t bm, int32_t bn) {
+  if (ls::gemm_tile_override(bm, bn) != 0) return fail(LS_ERR_SHAPE, "tile sizes must be 256 or 192 (0, 0: automatic)");
+  return LS_OK;
+}
+
 int ls_gemm_tn(int64_t M, int64_t N, int64_t K, const ls_bf16* A, const ls_bf16* B, float* C, int accumulate,
                void* stream) {
   ls::GemmArgs g;

@@ -1,12 +1,17 @@
 // bf16 matrix products on gfx950 matrix cores (v_mfma_f32_32x32x16_bf16) with
 // fp32 accumulation and fused epilogues for the decoder block.
 //
-// One workgroup of 4 waves computes a 256x256 tile of C; each wave owns a
-// 128x128 quarter (16 MFMA blocks of 32x32, accumulators in AGPRs).  Operand
-// tiles of 64 k-values move global -> LDS with buffer loads that write LDS
-// directly (16 bytes per lane, no staging registers) and return zero outside
-// the operand, so ragged edges need no branches.  Two LDS stages of 64 KB:
-// tile k+1 is in flight while the matrix cores consume tile k.
+// One workgroup of 4 waves computes a BM x BN tile of C (256 or 192 on each
+// side); each wave owns a quarter (up to 16 MFMA blocks of 32x32, accumulators
+// in AGPRs).  Operand tiles of 64 k-values move global -> LDS with buffer loads
+// that write LDS directly (16 bytes per lane, no staging registers) and return
+// zero outside the operand, so ragged edges need no branches.  Two LDS stages
+// of 64 KB: tile k+1 is in flight while the matrix cores consume tile k.
+//
+// The tile shape is picked per launch: on 256 compute units an 8192 x 3072
+// output is 384 tiles of 256 x 256 (one and a half waves of workgroups) but
+// exactly 512 tiles of 256 x 192, so the launcher estimates waves x tile area
+// for each shape the epilogue allows and takes the smallest.
 //
 // The tile depth is set by the load path: a k-contiguous operand row
 // contributes KT*2 bytes per tile, and the buffer->LDS path moves 128-byte row
@@ -17,10 +22,12 @@
 // the fragment reads free of bank conflicts):
 //   k-contiguous operand  [256 rows][64 k]  128-byte rows, chunk c of row r at
 //                         slot c ^ ((r/2) % 8); fragments are 16-byte reads.
-//   k-strided operand     [64 k][256 cols]  512-byte rows, chunk c of row k at
-//                         slot c ^ 4(k % 4); fragments are two transposing
-//                         8-byte reads (ds_read_b64_tr_b16), which hand each
-//                         lane 4 consecutive k of one column.
+//   k-strided operand     [64 k][W cols], W = 256 or 192: k-rows 2j and 2j+1 fill
+//                         the 1 KB block j (at bytes 0 and 2W; for W = 192 the
+//                         last 256 bytes of a block are padding), chunk c of
+//                         row k at slot c ^ ks_swz(k); fragments are two
+//                         transposing 8-byte reads (ds_read_b64_tr_b16), which
+//                         hand each lane 4 consecutive k of one column.
 // So every layout (forward, input-gradient and weight-gradient products)
 // runs the same matrix-core loop without any explicit transpose.
 //
@@ -28,6 +35,8 @@
 // its second, so that a lane ends up holding four consecutive output columns
 // of one row: 8-byte bf16 / 16-byte fp32 stores, and the RoPE and SwiGLU
 // partners of a column sit in the same lane.
+#include <atomic>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -36,13 +45,10 @@ namespace ls {
 
 namespace {
 
-constexpr int BM = 256, BN = 256, KT = 64;  // tile
+constexpr int KT = 64;                      // tile depth
 constexpr int KSTEPS = KT / 16;             // MFMA k-steps per tile
-constexpr int WGM = 2, WGN = 2;             // waves
-constexpr int NT = 64 * WGM * WGN;
-constexpr int WM = BM / WGM, WN = BN / WGN;
-constexpr int TM = WM / 32, TN = WN / 32;
-constexpr int TILE_ELEMS = 256 * KT;        // one operand tile in LDS (32 KB)
+constexpr int NT = 256;                     // 4 waves, 2 x 2 over the tile
+constexpr int TILE_ELEMS = 256 * KT;        // LDS region of one operand tile (32 KB)
 constexpr int GROUP_M = 8;                  // tile rows per group in the launch order
 constexpr int EPI_ROPE64 = 100;             // EPI_ROPE for 64-wide heads
 constexpr uint32_t OOB = LS_OOB;
@@ -71,11 +77,22 @@ LS_DEV void map_tile(int wg, int tiles_m, int tiles_n, int& tm, int& tn) {
 //    reads at one logical chunk must land on 16 distinct 16-byte bank groups of
 //    a 256-byte window; r % 2 picks the row's half of the window, (r/2) % 8
 //    the slot.
-//  - k-strided tiles (512-byte rows): a 32-lane transposing read covers 4
-//    rows x 64 bytes; XOR with 4 * (k % 4) puts the 4 rows' 64-byte runs on
-//    distinct quarters of a 256-byte window.
+//  - k-strided tiles: a 32-lane transposing read covers 4 consecutive k-rows
+//    (4-aligned) x 64 bytes.  With W = 256 the rows are 512 bytes apart, all at
+//    the same offset of a 256-byte window, and XOR with 4 * (k % 4) puts their
+//    64-byte runs on distinct quarters.  With W = 192 the rows sit at window
+//    offsets 0, 128, 0, 128 (384-byte rows, two per 1 KB block), and XOR with
+//    4 * ((k/2) % 2) moves the second pair by 64 bytes.
 LS_DEV int kc_swz(int r) { return (r >> 1) & 7; }
-LS_DEV int ks_swz(int k) { return 4 * (k & 3); }
+template <int W>
+LS_DEV int ks_swz(int k) {
+  return W == 256 ? 4 * (k & 3) : 4 * ((k >> 1) & 1);
+}
+// Element offset of (k-row kk, column col) in a k-strided tile of width W.
+template <int W>
+LS_DEV int ks_off(int kk, int col) {
+  return (kk >> 1) * 512 + (kk & 1) * W + 8 * ((col >> 3) ^ ks_swz<W>(kk)) + (col & 7);
+}
 
 LS_DEV float silu_f(float g) { return g * __frcp_rn(1.0f + __expf(-g)); }
 
@@ -137,21 +154,24 @@ LS_DEV void dma_kc(const Segs g, const bf16_t* gate, const bf16_t* up, int glu_r
 }
 
 // One load instruction of a 64-k tile of a k-strided operand (k rows k0 ..
-// k0+63, columns col0 .. col0+255 of `cols`); a wave issues jj = 0..7.
-// Instruction j = wave + 4jj fills k-rows 2j and 2j+1; lane l writes slot l%32
-// of k-row 2j + l/32 with that row's logical chunk (l%32) ^ ks_swz(k-row).
-// Segment starts are even.
+// k0+63, columns col0 .. col0+W-1 of `cols`); a wave issues jj = 0..7.
+// Instruction j = wave + 4jj fills k-rows 2j and 2j+1 (the 1 KB block j): lane
+// l < 2 W/8 writes slot l % (W/8) of k-row 2j + l / (W/8) with that row's
+// logical chunk slot ^ ks_swz(k-row); the remaining lanes of a 192-wide tile
+// load zeros into the block's padding.  Segment starts are even.
+template <int W>
 LS_DEV void dma_ks(const Segs g, int col0, int cols, int k0, int K, bf16_t* lds, int wave, int lane, int jj) {
-  const int lh = lane >> 5;
+  constexpr int CPR = W / 8;  // chunks per k-row
   const int j = wave + 4 * jj;
-  const int kb = k0 + 2 * j;  // first k row of the instruction (uniform)
+  const int half = lane / CPR;  // 0 or 1 (2: padding lanes)
+  const int kb = k0 + 2 * j;    // first k row of the instruction (uniform)
   int s0;
   const i32x4 r = seg_rsrc(g, kb, s0);
-  const int c = (lane & 31) ^ ks_swz(2 * j + lh);
+  const int c = (lane % CPR) ^ ks_swz<W>(2 * j + half);
   const int col = col0 + 8 * c;
-  const int lk = kb - s0 + lh;
-  const uint32_t voff = (kb + lh < K && col < cols) ? (uint32_t)(lk * g.ld * 2 + col * 2) : OOB;
-  dma16(r, voff, lds + j * 512);
+  const int lk = kb - s0 + half;
+  const bool ok = half < 2 && kb + half < K && col < cols;
+  dma16(r, ok ? (uint32_t)(lk * g.ld * 2 + col * 2) : OOB, lds + j * 512);
 }
 
 // Fragment of a k-contiguous tile: lane gets row `r` (tile-local), k = 16s + 8*(lane/32) .. +7.
@@ -159,8 +179,10 @@ LS_DEV u32x4 frag_kc(const bf16_t* lds, int r, int s, int lh) {
   return *(const u32x4*)(lds + r * KT + 8 * ((2 * s + lh) ^ kc_swz(r)));
 }
 
-// Fragment of a k-strided tile for the 32 columns starting at c32 (tile-local):
-// lane gets column c32 + lane%32, k = 16s + 8*(lane/32) .. +7, via two transposing reads.
+// Fragment of a k-strided tile (width W) for the 32 columns starting at c32
+// (tile-local): lane gets column c32 + lane%32, k = 16s + 8*(lane/32) .. +7,
+// via two transposing reads.
+template <int W>
 LS_DEV u32x4 frag_ks(const bf16_t* lds, int c32, int s, int lane) {
   const int g = lane >> 4, q = lane & 15;
   const int col = c32 + 16 * (g & 1) + 4 * (q & 3);
@@ -168,8 +190,7 @@ LS_DEV u32x4 frag_ks(const bf16_t* lds, int c32, int s, int lane) {
 #pragma unroll
   for (int t = 0; t < 2; ++t) {
     const int kk = 16 * s + 8 * (g >> 1) + 4 * t + (q >> 2);
-    const bf16_t* p = lds + kk * 256 + 8 * ((col >> 3) ^ ks_swz(kk)) + (col & 7);
-    const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS s16x4*)p);
+    const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS s16x4*)(lds + ks_off<W>(kk, col)));
     const u32x2 w = __builtin_bit_cast(u32x2, v);
     out[2 * t] = w[0];
     out[2 * t + 1] = w[1];
@@ -177,15 +198,18 @@ LS_DEV u32x4 frag_ks(const bf16_t* lds, int c32, int s, int lane) {
   return out;
 }
 
-template <bool AK, bool BKC, int EPI>
+template <bool AK, bool BKC, int EPI, int BM, int BN>
 __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
+  constexpr int WM = BM / 2, WN = BN / 2;  // wave tile
+  constexpr int TM = WM / 32, TN = WN / 32;
+  constexpr int NA = AK ? BM / 32 : 8, NB = BKC ? BN / 32 : 8;  // load instructions per wave and tile
   // Two LDS stages of [A tile | B tile].  The buffer->LDS loads are inline
   // assembly the compiler does not see, so the stage can be picked at run time.
   __shared__ __attribute__((aligned(1024))) bf16_t lds[2][2 * TILE_ELEMS];
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int wm = wave / WGN, wn = wave % WGN;
+  const int wm = wave / 2, wn = wave % 2;
   const int tiles_m = (p.M + BM - 1) / BM, tiles_n = (p.N + BN - 1) / BN;
   int tm, tn;
   map_tile(blockIdx.x, tiles_m, tiles_n, tm, tn);
@@ -208,15 +232,18 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
 
   const bf16_t* gate = p.B[0];
   const bf16_t* up = p.B[1];
-  // Load instruction q (0..15) of tile kt into stage st: q < 8 are the A tile's, the rest B's.
-  auto issue = [&](int kt, bf16_t* st, int q) {
+  // The NA + NB load instructions of tile kt into stage st.
+  auto issue = [&](int kt, bf16_t* st) {
     const int k0 = kt * KT;
-    if (q < 8) {
+#pragma unroll
+    for (int q = 0; q < NA; ++q) {
       if constexpr (AK) dma_kc<false>(ga, nullptr, nullptr, 0, m0, k0, K, st, wave, lane, q);
-      else dma_ks(ga, m0, p.M, k0, K, st, wave, lane, q);
-    } else {
-      if constexpr (BKC) dma_kc<EPI == EPI_GLU_FWD>(gb, gate, up, p.glu_rows, n0, k0, K, st + TILE_ELEMS, wave, lane, q - 8);
-      else dma_ks(gb, n0, p.N, k0, K, st + TILE_ELEMS, wave, lane, q - 8);
+      else dma_ks<BM>(ga, m0, p.M, k0, K, st, wave, lane, q);
+    }
+#pragma unroll
+    for (int q = 0; q < NB; ++q) {
+      if constexpr (BKC) dma_kc<EPI == EPI_GLU_FWD>(gb, gate, up, p.glu_rows, n0, k0, K, st + TILE_ELEMS, wave, lane, q);
+      else dma_ks<BN>(gb, n0, p.N, k0, K, st + TILE_ELEMS, wave, lane, q);
     }
   };
 
@@ -244,10 +271,10 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
     const bf16_t* bs = lds[stage] + TILE_ELEMS;
 #pragma unroll
     for (int i = 0; i < TM; ++i)
-      af[buf][i] = AK ? frag_kc(as, wm * WM + 32 * i + lr, s, lh) : frag_ks(as, wm * WM + 32 * i, s, lane);
+      af[buf][i] = AK ? frag_kc(as, wm * WM + 32 * i + lr, s, lh) : frag_ks<BM>(as, wm * WM + 32 * i, s, lane);
 #pragma unroll
     for (int j = 0; j < TN; ++j)
-      bfr[buf][j] = BKC ? frag_kc(bs, wn * WN + 32 * j + lr, s, lh) : frag_ks(bs, wn * WN + 32 * j, s, lane);
+      bfr[buf][j] = BKC ? frag_kc(bs, wn * WN + 32 * j + lr, s, lh) : frag_ks<BN>(bs, wn * WN + 32 * j, s, lane);
   };
   auto mfmas = [&](int buf) {
 #pragma unroll
@@ -257,16 +284,12 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
   };
   auto sync_tile = []() { sync_lds(); };
 
-#pragma unroll
-  for (int q = 0; q < 16; ++q) issue(0, lds[0], q);
+  issue(0, lds[0]);
   sync_tile();
   load_frags(0, 0, 0);
   for (int kk = 0; kk < nk; ++kk) {
     const int cur = kk & 1;
-    if (kk + 1 < nk) {
-#pragma unroll
-      for (int q = 0; q < 16; ++q) issue(kk + 1, lds[cur ^ 1], q);
-    }
+    if (kk + 1 < nk) issue(kk + 1, lds[cur ^ 1]);
 #pragma unroll
     for (int s = 0; s < KSTEPS; ++s) {
       const int buf = s & 1;
@@ -286,48 +309,48 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
   // ---- epilogue ---------------------------------------------------------------
   // Lane holds C[32i + lr][32j + 8q + 4lh .. +3] of its wave tile (acc[i][j][4q..]).
   // Results go through a 32 KB LDS region per wave so that global loads and
-  // stores move whole 256-byte row segments (16 bytes per lane).  Staging rows
-  // are unpadded (bf16: 128 rows x 256 B, fp32: 64 rows x 512 B) with the
-  // 16-byte chunk index XOR-swizzled by the row, so the column-wise writes
-  // from the MFMA layout and the row-wise reads both avoid bank conflicts.
+  // stores move whole row segments (16 bytes per lane).  Staging rows have a
+  // fixed pitch (bf16: 128 columns = 256 B, up to 128 rows; fp32: 128 columns =
+  // 512 B, 32 rows) with the 16-byte chunk index XOR-swizzled by the row, so the
+  // column-wise writes from the MFMA layout and the row-wise reads both avoid
+  // bank conflicts; a 96-wide wave tile uses 12 of the 16 (24 of the 32) chunks.
   bf16_t* stg = &lds[wave >> 1][(wave & 1) * TILE_ELEMS];  // 32 KB per wave
   float* stgf = (float*)stg;
   auto sb = [](int r, int col) { return r * 128 + ((((col >> 3) ^ (r & 15)) << 3) | (col & 7)); };
   auto sf = [](int r, int col) { return r * 128 + ((((col >> 2) ^ (r & 31)) << 2) | (col & 3)); };
   const int mw = m0 + wm * WM, nw = n0 + wn * WN;
 
-  // bf16 staging: 128 rows x 128 columns -> rows of `dst` (row-major, ld), at columns col(cc)
+  // bf16 staging: WM rows x WN columns -> rows of `dst` (row-major, ld) from column col0
   auto put4 = [&](int r, int c, const float v[4]) {
     *(u32x2*)&stg[sb(r, c)] = u32x2{pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3])};
   };
   auto flush_bf16 = [&](bf16_t* dst, int64_t ldd, int col0, int ncols_valid) {
 #pragma unroll 4
-    for (int t = 0; t < 32; ++t) {
+    for (int t = 0; t < WM / 4; ++t) {
       const int c = lane + 64 * t, r = c >> 4, cc = c & 15;
       const u32x4 v = *(const u32x4*)&stg[sb(r, cc * 8)];
-      if (mw + r < p.M && cc * 8 < ncols_valid) *(u32x4*)(dst + (int64_t)(mw + r) * ldd + col0 + cc * 8) = v;
+      if (cc < WN / 8 && mw + r < p.M && cc * 8 < ncols_valid)
+        *(u32x4*)(dst + (int64_t)(mw + r) * ldd + col0 + cc * 8) = v;
     }
   };
 
   if constexpr (EPI == EPI_F32 || EPI == EPI_RESID) {
-    // fp32 staging in two halves of 64 rows; the residual / old gradient is read coalesced.
+    // fp32 staging per 32-row block; the residual / old gradient is read coalesced.
+    constexpr int CH = WN / 4;  // 16-byte chunks per staged row
 #pragma unroll
-    for (int half = 0; half < 2; ++half) {
+    for (int i = 0; i < TM; ++i) {
 #pragma unroll
-      for (int ii = 0; ii < 2; ++ii)
+      for (int j = 0; j < TN; ++j)
 #pragma unroll
-        for (int j = 0; j < TN; ++j)
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const f32x4 v = {acc[2 * half + ii][j][4 * q], acc[2 * half + ii][j][4 * q + 1],
-                             acc[2 * half + ii][j][4 * q + 2], acc[2 * half + ii][j][4 * q + 3]};
-            *(f32x4*)&stgf[sf(32 * ii + lr, 32 * j + 8 * q + 4 * lh)] = v;
-          }
+        for (int q = 0; q < 4; ++q) {
+          const f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+          *(f32x4*)&stgf[sf(lr, 32 * j + 8 * q + 4 * lh)] = v;
+        }
 #pragma unroll 4
-      for (int t = 0; t < 32; ++t) {
-        const int c = lane + 64 * t, r = c >> 5, cc = c & 31;
+      for (int t = 0; t < CH / 2; ++t) {
+        const int c = lane + 64 * t, r = c / CH, cc = c % CH;
         f32x4 v = *(const f32x4*)&stgf[sf(r, cc * 4)];
-        const int m = mw + 64 * half + r, n = nw + cc * 4;
+        const int m = mw + 32 * i + r, n = nw + cc * 4;
         if (m < p.M && n < p.N) {
           if constexpr (EPI == EPI_F32) {
             const int sg = m >= p.f_start[2] ? 2 : (m >= p.f_start[1] ? 1 : 0);
@@ -392,6 +415,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
       if (mw + r < p.M && cc * 8 < nvalid) *(u32x4*)(p.act + (int64_t)(mw + r) * p.glu_I + col0 + cc * 8) = v;
     }
   } else if constexpr (EPI == EPI_GLU_BWD) {
+    static_assert(WN == 128, "the gate/up staging covers 128-column wave tiles");
     // acc = dact.  Per 32-row block: the saved gate and up values are read
     // coalesced into LDS, dg = dact u silu'(g) and du = dact silu(g) replace
     // them in place, and both go out coalesced.
@@ -493,33 +517,97 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
   }
 }
 
-template <bool AK, bool BKC, int EPI>
+template <bool AK, bool BKC, int EPI, int BM, int BN>
 hipError_t launch(const GemmArgs& a, hipStream_t s) {
   const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_kernel<AK, BKC, EPI>), dim3(tiles), dim3(NT), 0, s, a);
+  hipLaunchKernelGGL((gemm_kernel<AK, BKC, EPI, BM, BN>), dim3(tiles), dim3(NT), 0, s, a);
   return hipGetLastError();
+}
+
+int compute_units() {
+  static const int n = [] {
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        v <= 0)
+      v = 256;
+    return v;
+  }();
+  return n;
+}
+
+std::atomic<int> g_tile_override{0};  // 0: automatic, else 1000 * BM + BN
+
+// Tile shape (1000 * BM + BN) of a launch: among the shapes the kernel variant
+// allows, the one with the fewest waves of workgroups times tile area; a
+// 192-wide side counts 10% extra for its higher LDS traffic per flop.
+int pick_tile(int M, int N, bool m192, bool n192) {
+  const int forced = g_tile_override.load(std::memory_order_relaxed);
+  if (forced) {
+    const int bm = forced / 1000, bn = forced % 1000;
+    return (bm == 256 || m192) && (bn == 256 || n192) ? forced : 256256;
+  }
+  const int ncu = compute_units();
+  double best = 0.0;
+  int code = 0;
+  for (int bm : {256, 192}) {
+    if (bm == 192 && !m192) continue;
+    for (int bn : {256, 192}) {
+      if (bn == 192 && !n192) continue;
+      const int64_t tiles = (int64_t)((M + bm - 1) / bm) * ((N + bn - 1) / bn);
+      const double cost = (double)((tiles + ncu - 1) / ncu) * bm * bn * (bm == 256 ? 1.0 : 1.1) * (bn == 256 ? 1.0 : 1.1);
+      if (code == 0 || cost < best) {
+        best = cost;
+        code = bm * 1000 + bn;
+      }
+    }
+  }
+  return code;
 }
 
 }  // namespace
 
+int gemm_tile_override(int bm, int bn) {
+  if (bm == 0 && bn == 0) {
+    g_tile_override.store(0);
+    return 0;
+  }
+  if ((bm != 256 && bm != 192) || (bn != 256 && bn != 192)) return -1;
+  g_tile_override.store(bm * 1000 + bn);
+  return 0;
+}
+
 hipError_t gemm(const GemmArgs& a, hipStream_t s) {
   if (a.a_kcontig && a.b_kcontig) {
     switch (a.epi) {
-      case EPI_BF16: return launch<true, true, EPI_BF16>(a, s);
-      case EPI_RESID: return launch<true, true, EPI_RESID>(a, s);
+      case EPI_BF16:
+        return pick_tile(a.M, a.N, false, true) == 256192 ? launch<true, true, EPI_BF16, 256, 192>(a, s)
+                                                          : launch<true, true, EPI_BF16, 256, 256>(a, s);
+      case EPI_RESID:
+        return pick_tile(a.M, a.N, false, true) == 256192 ? launch<true, true, EPI_RESID, 256, 192>(a, s)
+                                                          : launch<true, true, EPI_RESID, 256, 256>(a, s);
       case EPI_ROPE:
-        return a.head_dim == 64 ? launch<true, true, EPI_ROPE64>(a, s) : launch<true, true, EPI_ROPE>(a, s);
-      case EPI_GLU_FWD: return launch<true, true, EPI_GLU_FWD>(a, s);
+        return a.head_dim == 64 ? launch<true, true, EPI_ROPE64, 256, 256>(a, s)
+                                : launch<true, true, EPI_ROPE, 256, 256>(a, s);
+      case EPI_GLU_FWD: return launch<true, true, EPI_GLU_FWD, 256, 256>(a, s);
       default: break;
     }
   } else if (a.a_kcontig && !a.b_kcontig) {
     switch (a.epi) {
-      case EPI_BF16: return launch<true, false, EPI_BF16>(a, s);
-      case EPI_GLU_BWD: return launch<true, false, EPI_GLU_BWD>(a, s);
+      case EPI_BF16:
+        return pick_tile(a.M, a.N, false, true) == 256192 ? launch<true, false, EPI_BF16, 256, 192>(a, s)
+                                                          : launch<true, false, EPI_BF16, 256, 256>(a, s);
+      case EPI_GLU_BWD: return launch<true, false, EPI_GLU_BWD, 256, 256>(a, s);
       default: break;
     }
   } else if (!a.a_kcontig && !a.b_kcontig) {
-    if (a.epi == EPI_F32) return launch<false, false, EPI_F32>(a, s);
+    if (a.epi == EPI_F32) {
+      switch (pick_tile(a.M, a.N, true, true)) {
+        case 192192: return launch<false, false, EPI_F32, 192, 192>(a, s);
+        case 192256: return launch<false, false, EPI_F32, 192, 256>(a, s);
+        case 256192: return launch<false, false, EPI_F32, 256, 192>(a, s);
+        default: return launch<false, false, EPI_F32, 256, 256>(a, s);
+      }
+    }
   }
   return hipErrorInvalidValue;
 }

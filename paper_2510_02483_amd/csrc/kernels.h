@@ -54,6 +54,9 @@ struct GemmArgs {
 };
 
 hipError_t gemm(const GemmArgs& a, hipStream_t s);
+// Force the tile shape of later gemm launches (bm, bn in {256, 192}; 0, 0 =
+// automatic).  Variants that only exist as 256 x 256 ignore it.  -1 on bad sizes.
+int gemm_tile_override(int bm, int bn);
 
 // ---- RMSNorm ------------------------------------------------------------------
 hipError_t rmsnorm_fwd(int64_t rows, int hidden, float eps, const bf16_t* x, const bf16_t* gamma,

@@ -69,6 +69,7 @@ _PROTOS = {
     "ls_gemm_nt": (ctypes.c_int, [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, _P, _P, _P, _P]),
     "ls_gemm_nn": (ctypes.c_int, [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, _P, _P, _P, _P]),
     "ls_gemm_tn": (ctypes.c_int, [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, _P, _P, _P, ctypes.c_int, _P]),
+    "ls_gemm_tile_override": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32]),
     "ls_timing_begin": (ctypes.c_int, [ctypes.c_char_p, ctypes.c_int]),
     "ls_timing_end": (ctypes.c_int, [_P, _P]),
 }
@@ -204,6 +205,11 @@ def ls_gemm_nn(A, B, C, stream=None):
     M, K = A.shape
     N = B.shape[1]
     _check(lib().ls_gemm_nn(M, N, K, _p(A), _p(B), _p(C), _stream(stream)), "ls_gemm_nn")
+
+
+def ls_gemm_tile_override(bm=0, bn=0):
+    """Force the matrix-product tile shape (256 or 192 per side); (0, 0) = automatic."""
+    _check(lib().ls_gemm_tile_override(int(bm), int(bn)), "ls_gemm_tile_override")
 
 
 def ls_gemm_tn(A, B, C, accumulate=False, stream=None):

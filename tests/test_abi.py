@@ -120,3 +120,11 @@ def test_gemm_and_norm_argument_checks():
     assert need >= 64 * 4
     assert lib.ls_rmsnorm_bwd(100, 64, V(1 << 32), V(1 << 33), V(1 << 34), V(1 << 35), None, V(1 << 36),
                               V(1 << 37), 0, V(1 << 38), need - 4, None) == 6
+
+
+def test_gemm_tile_override_arguments():
+    lib = L.lib()
+    assert lib.ls_gemm_tile_override(100, 256) == 2
+    assert lib.ls_gemm_tile_override(256, 128) == 2
+    assert lib.ls_gemm_tile_override(192, 256) == 0
+    assert lib.ls_gemm_tile_override(0, 0) == 0

@@ -14,13 +14,23 @@ from gpu_util import GRAD_TOL, OUT_TOL, bf16_randn, f64, fro_rel, max_rel, need_
 
 pytestmark = pytest.mark.gpu
 
-GEMM_SHAPES = [(136, 264, 72), (520, 776, 1000), (256, 512, 640), (8, 8, 8), (1032, 264, 1376)]
+GEMM_SHAPES = [(136, 264, 72), (520, 776, 1000), (256, 512, 640), (8, 8, 8), (1032, 264, 1376), (392, 584, 200)]
+# workgroup tile shapes: automatic choice, then each forced shape (products
+# whose kernel has no such variant fall back to 256 x 256)
+GEMM_TILES = [(0, 0), (256, 256), (256, 192), (192, 256), (192, 192)]
+
+
+@pytest.fixture(params=GEMM_TILES, ids=lambda t: "auto" if t == (0, 0) else f"{t[0]}x{t[1]}")
+def tile(request):
+    L.ls_gemm_tile_override(*request.param)
+    yield request.param
+    L.ls_gemm_tile_override(0, 0)
 
 
 @pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
-def test_gemm_nt(M, N, K):
+def test_gemm_nt(M, N, K, tile):
     need_gpu()
-    say(f"gemm_nt M={M} N={N} K={K}")
+    say(f"gemm_nt M={M} N={N} K={K} tile={tile}")
     A, B = bf16_randn((M, K), 1), bf16_randn((N, K), 2)
     C = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
     L.ls_gemm_nt(A, B, C)
@@ -30,9 +40,9 @@ def test_gemm_nt(M, N, K):
 
 
 @pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
-def test_gemm_nn(M, N, K):
+def test_gemm_nn(M, N, K, tile):
     need_gpu()
-    say(f"gemm_nn M={M} N={N} K={K}")
+    say(f"gemm_nn M={M} N={N} K={K} tile={tile}")
     A, B = bf16_randn((M, K), 3), bf16_randn((K, N), 4)
     C = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
     L.ls_gemm_nn(A, B, C)
@@ -41,9 +51,9 @@ def test_gemm_nn(M, N, K):
 
 
 @pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
-def test_gemm_tn_accumulate(M, N, K):
+def test_gemm_tn_accumulate(M, N, K, tile):
     need_gpu()
-    say(f"gemm_tn M={M} N={N} K={K}")
+    say(f"gemm_tn M={M} N={N} K={K} tile={tile}")
     A, B = bf16_randn((K, M), 5), bf16_randn((K, N), 6)
     C = torch.full((M, N), 0.5, dtype=torch.float32, device="cuda")
     L.ls_gemm_tn(A, B, C, accumulate=False)
