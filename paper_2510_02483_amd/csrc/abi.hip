@@ -21,6 +21,10 @@ constexpr int kVersion = 100;  // 0.1.0
 
 thread_local std::string g_last_error;
 
+// Largest matrix in bytes (exclusive): the kernels' buffer resources are
+// clamped to 2047 MiB.
+constexpr int64_t kMaxBytes = (int64_t)0x7ff00000;
+
 int fail(int code, const char* fmt, ...) {
   char buf[512];
   va_list ap;
@@ -108,11 +112,12 @@ int check_cfg(const ls_block_cfg* c) {
   if (c->hidden > 8192) return fail(LS_ERR_UNSUPPORTED, "hidden %d exceeds 8192", c->hidden);
   const Dims m = dims_of(*c);
   const int64_t lim = (int64_t)1 << 30;
-  // every matrix is addressed with 32-bit byte offsets (buffer loads)
+  // every matrix is addressed with 32-bit byte offsets (buffer loads, whose
+  // resources stay below 2047 MiB)
   const int64_t widest = std::max(std::max(m.Dqkv, 2 * m.I), m.H);
-  if (m.T >= lim || m.Dqkv >= lim || 2 * m.I >= lim || m.T * widest * 2 >= ((int64_t)1 << 31) ||
-      m.I * m.H * 2 >= ((int64_t)1 << 31) || m.Dqkv * m.H * 2 >= ((int64_t)1 << 31))
-    return fail(LS_ERR_SHAPE, "problem too large (a matrix reaches 2 GiB)");
+  if (m.T >= lim || m.Dqkv >= lim || 2 * m.I >= lim || m.T * widest * 2 >= kMaxBytes ||
+      m.I * m.H * 2 >= kMaxBytes || m.Dqkv * m.H * 2 >= kMaxBytes)
+    return fail(LS_ERR_SHAPE, "problem too large (a matrix reaches 2047 MiB)");
   return LS_OK;
 }
 
@@ -818,8 +823,8 @@ static int check_gemm(int64_t M, int64_t N, int64_t K) {
   if (M <= 0 || N <= 0 || K <= 0) return fail(LS_ERR_SHAPE, "M, N, K must be positive");
   if (M % 8 || N % 8 || K % 8) return fail(LS_ERR_SHAPE, "M, N, K must be multiples of 8");
   if (M >= (1 << 30) || N >= (1 << 30) || K >= (1 << 30)) return fail(LS_ERR_SHAPE, "dimension too large");
-  if (M * K * 2 >= ((int64_t)1 << 31) || K * N * 2 >= ((int64_t)1 << 31) || M * N * 4 >= ((int64_t)1 << 31))
-    return fail(LS_ERR_SHAPE, "an operand reaches 2 GiB");
+  if (M * K * 2 >= kMaxBytes || K * N * 2 >= kMaxBytes || M * N * 4 >= kMaxBytes)
+    return fail(LS_ERR_SHAPE, "an operand reaches 2047 MiB");
   return LS_OK;
 }
 

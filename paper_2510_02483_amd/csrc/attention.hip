@@ -79,20 +79,22 @@ LS_DEV int tile_swz(int r) {
 // Load rows row0 .. row0+ROWS-1, columns col0 .. col0+D-1 of a row-major bf16
 // matrix (leading dimension ld elements, `rows` rows, covered by the buffer
 // resource r) into an LDS tile; rows at or past `rows` read as zero.  Each
-// instruction fills 1 KB of the tile (64/(D/8) rows); the 4 waves share them.
+// load fills 1 KB of the tile (64/(D/8) rows); wave w fills the consecutive
+// blocks w*PER .. w*PER+PER-1 with one M0 write.
 template <int D, int ROWS>
 LS_DEV void load_tile(i32x4 r, int64_t ld, int row0, int rows, int col0, bf16_t* t, int wave, int lane) {
-  constexpr int CPR = D / 8, RPI = 64 / CPR, NI = ROWS / RPI;
-  static_assert(NI % 4 == 0, "instructions split evenly over 4 waves");
+  constexpr int CPR = D / 8, RPI = 64 / CPR, NI = ROWS / RPI, PER = NI / 4;
+  static_assert(NI % 4 == 0 && (PER == 2 || PER == 4), "loads split evenly over 4 waves in groups of 2 or 4");
+  DmaLoad l[PER];
 #pragma unroll
-  for (int jj = 0; jj < NI / 4; ++jj) {
-    const int j = wave + 4 * jj;
+  for (int jj = 0; jj < PER; ++jj) {
+    const int j = wave * PER + jj;
     const int rr = j * RPI + lane / CPR;
     const int c = (lane % CPR) ^ tile_swz<D>(rr);
     const int gr = row0 + rr;
-    const uint32_t voff = gr < rows ? (uint32_t)(((int64_t)gr * ld + col0 + 8 * c) * 2) : LS_OOB;
-    dma16(r, voff, t + j * 512);
+    l[jj] = DmaLoad{r, gr < rows ? (uint32_t)(((int64_t)gr * ld + col0 + 8 * c) * 2) : LS_OOB};
   }
+  dma16_group<PER>(l, t + wave * PER * 512);
 }
 
 // 64 floats v[i0 .. i0+63] of a buffer of `n` floats (resource r; entries at or

@@ -60,7 +60,22 @@ LS_DEV i32x4 rsrc(const void* base, uint32_t bytes) {
                (int32_t)__builtin_amdgcn_readfirstlane(bytes), 0x00020000};
 }
 
-LS_DEV uint32_t clamp_bytes(int64_t b) { return b <= 0 ? 0u : (b >= 0x7fffffff ? 0x7fffffffu : (uint32_t)b); }
+// Buffer sizes are clamped below 2^31 - 1 MB, so that LS_OOB plus any
+// instruction offset stays outside every (possibly shifted, see dma16_group)
+// resource.  The C ABI rejects buffers of 2 GiB and more.
+LS_DEV uint32_t clamp_bytes(int64_t b) { return b <= 0 ? 0u : (b >= 0x7ff00000 ? 0x7ff00000u : (uint32_t)b); }
+
+// One 16-byte-per-lane buffer->LDS load: resource and per-lane byte offset.
+struct DmaLoad {
+  i32x4 r;
+  uint32_t voff;
+};
+
+// LDS byte address of a generic pointer into LDS: a generic LDS address is the
+// LDS aperture in the high 32 bits and the LDS address in the low 32 bits.
+// (Taken from the bits rather than through an address-space cast, whose null
+// check the compiler folds into an invalid instruction in some kernels.)
+LS_DEV uint32_t lds_offset(const void* p) { return (uint32_t)(uintptr_t)p; }
 
 // 16 bytes per lane from a buffer (zero outside it) straight into LDS: lane l's
 // bytes land at lds + 16 l (the address is uniform over the wave).  Issued as
@@ -68,11 +83,52 @@ LS_DEV uint32_t clamp_bytes(int64_t b) { return b <= 0 ? 0u : (b >= 0x7fffffff ?
 // otherwise make every later LDS read wait for all loads in flight.  The
 // caller orders the LDS reads with explicit vmcnt waits and barriers.
 LS_DEV void dma16(i32x4 r, uint32_t voff, const void* lds) {
-  const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(const LDS_AS void*)lds);
+  const uint32_t m0 = __builtin_amdgcn_readfirstlane(lds_offset(lds));
   asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
                :
                : "s"(m0), "v"(voff), "s"(r)
                : "memory", "m0");
+}
+
+// N (1..4) buffer->LDS loads into the consecutive 1 KB LDS blocks lds,
+// lds + 1 KB, ... with a single M0 write: each M0 write waits for the loads
+// before it to leave the issue stage, so writing it once per load serialises
+// the wave.  Load i carries the instruction offset i KB, which the hardware
+// adds to both its LDS and its memory address, so its resource is moved back
+// by i KB (base - i KB, size + i KB) to read the same bytes.
+template <int N>
+LS_DEV void dma16_group(DmaLoad (&l)[N], const void* lds) {
+#pragma unroll
+  for (int i = 1; i < N; ++i) {
+    const uint64_t base = ((uint64_t)(uint32_t)l[i].r[1] << 32 | (uint32_t)l[i].r[0]) - 1024u * i;
+    l[i].r[0] = (int32_t)(uint32_t)base;
+    l[i].r[1] = (int32_t)((uint32_t)(base >> 32) & 0xffffu);
+    l[i].r[2] = (int32_t)((uint32_t)l[i].r[2] + 1024u * i);
+  }
+  const uint32_t m0 = __builtin_amdgcn_readfirstlane(lds_offset(lds));
+  if constexpr (N == 4) {
+    asm volatile(
+        "s_mov_b32 m0, %0\n\ts_nop 0\n\t"
+        "buffer_load_dwordx4 %1, %5, 0 offen lds\n\t"
+        "buffer_load_dwordx4 %2, %6, 0 offen offset:1024 lds\n\t"
+        "buffer_load_dwordx4 %3, %7, 0 offen offset:2048 lds\n\t"
+        "buffer_load_dwordx4 %4, %8, 0 offen offset:3072 lds"
+        :
+        : "s"(m0), "v"(l[0].voff), "v"(l[1].voff), "v"(l[2].voff), "v"(l[3].voff), "s"(l[0].r), "s"(l[1].r),
+          "s"(l[2].r), "s"(l[3].r)
+        : "memory", "m0");
+  } else if constexpr (N == 2) {
+    asm volatile(
+        "s_mov_b32 m0, %0\n\ts_nop 0\n\t"
+        "buffer_load_dwordx4 %1, %3, 0 offen lds\n\t"
+        "buffer_load_dwordx4 %2, %4, 0 offen offset:1024 lds"
+        :
+        : "s"(m0), "v"(l[0].voff), "v"(l[1].voff), "s"(l[0].r), "s"(l[1].r)
+        : "memory", "m0");
+  } else {
+    static_assert(N == 1, "groups of 1, 2 or 4 loads");
+    dma16(l[0].r, l[0].voff, lds);
+  }
 }
 
 // Wait for every buffer->LDS load of this wave and every LDS access, then for

@@ -125,15 +125,13 @@ LS_DEV i32x4 seg_rsrc(const Segs g, int rb, int& seg_start) {
   return rsrc(base, clamp_bytes((int64_t)(s_end - s0) * g.ld * 2));
 }
 
-// One load instruction of a 64-k tile of a k-contiguous operand (rows row0 ..
-// row0+255, k0 .. k0+63); a wave issues jj = 0..7.  Instruction j = wave + 4jj
-// fills the 1 KB block j of the tile, i.e. rows 8j .. 8j+7; lane l writes slot
+// The load of 1 KB block j of a 64-k tile of a k-contiguous operand (rows
+// row0 .. row0+255 or +191, k0 .. k0+63): rows 8j .. 8j+7; lane l writes slot
 // l%8 of row 8j + l/8 with that row's logical chunk (l%8) ^ kc_swz(row), so the
 // 8 lanes of a row fetch its whole 128-byte piece.
 template <bool GLU>
-LS_DEV void dma_kc(const Segs g, const bf16_t* gate, const bf16_t* up, int glu_rows, int row0, int k0, int K,
-                   bf16_t* lds, int wave, int lane, int jj) {
-  const int j = wave + 4 * jj;
+LS_DEV DmaLoad kc_load(const Segs g, const bf16_t* gate, const bf16_t* up, int glu_rows, int row0, int k0, int K,
+                       int j, int lane) {
   const int rr = 8 * j + (lane >> 3);
   const int c = (lane & 7) ^ kc_swz(rr);
   const int k = k0 + 8 * c;
@@ -149,20 +147,17 @@ LS_DEV void dma_kc(const Segs g, const bf16_t* gate, const bf16_t* up, int glu_r
     lrow0 = rb - s0;
   }
   const int lrow = lrow0 + (lane >> 3);
-  const uint32_t voff = k < K ? (uint32_t)(lrow * g.ld * 2 + k * 2) : OOB;
-  dma16(r, voff, lds + j * 512);
+  return DmaLoad{r, k < K ? (uint32_t)(lrow * g.ld * 2 + k * 2) : OOB};
 }
 
-// One load instruction of a 64-k tile of a k-strided operand (k rows k0 ..
-// k0+63, columns col0 .. col0+W-1 of `cols`); a wave issues jj = 0..7.
-// Instruction j = wave + 4jj fills k-rows 2j and 2j+1 (the 1 KB block j): lane
+// The load of 1 KB block j of a 64-k tile of a k-strided operand (k rows k0 ..
+// k0+63, columns col0 .. col0+W-1 of `cols`): k-rows 2j and 2j+1; lane
 // l < 2 W/8 writes slot l % (W/8) of k-row 2j + l / (W/8) with that row's
 // logical chunk slot ^ ks_swz(k-row); the remaining lanes of a 192-wide tile
 // load zeros into the block's padding.  Segment starts are even.
 template <int W>
-LS_DEV void dma_ks(const Segs g, int col0, int cols, int k0, int K, bf16_t* lds, int wave, int lane, int jj) {
+LS_DEV DmaLoad ks_load(const Segs g, int col0, int cols, int k0, int K, int j, int lane) {
   constexpr int CPR = W / 8;  // chunks per k-row
-  const int j = wave + 4 * jj;
   const int half = lane / CPR;  // 0 or 1 (2: padding lanes)
   const int kb = k0 + 2 * j;    // first k row of the instruction (uniform)
   int s0;
@@ -171,7 +166,7 @@ LS_DEV void dma_ks(const Segs g, int col0, int cols, int k0, int K, bf16_t* lds,
   const int col = col0 + 8 * c;
   const int lk = kb - s0 + half;
   const bool ok = half < 2 && kb + half < K && col < cols;
-  dma16(r, ok ? (uint32_t)(lk * g.ld * 2 + col * 2) : OOB, lds + j * 512);
+  return DmaLoad{r, ok ? (uint32_t)(lk * g.ld * 2 + col * 2) : OOB};
 }
 
 // Fragment of a k-contiguous tile: lane gets row `r` (tile-local), k = 16s + 8*(lane/32) .. +7.
@@ -232,18 +227,42 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
 
   const bf16_t* gate = p.B[0];
   const bf16_t* up = p.B[1];
-  // The NA + NB load instructions of tile kt into stage st.
+  // The loads of tile kt into stage st: wave w fills the NA consecutive 1 KB
+  // blocks w*NA .. of the A tile and the NB blocks w*NB .. of the B tile, in
+  // groups of four (one M0 write per group).
+  auto load_a = [&](int k0, int j) -> DmaLoad {
+    if constexpr (AK) return kc_load<false>(ga, nullptr, nullptr, 0, m0, k0, K, j, lane);
+    else return ks_load<BM>(ga, m0, p.M, k0, K, j, lane);
+  };
+  auto load_b = [&](int k0, int j) -> DmaLoad {
+    if constexpr (BKC) return kc_load<EPI == EPI_GLU_FWD>(gb, gate, up, p.glu_rows, n0, k0, K, j, lane);
+    else return ks_load<BN>(gb, n0, p.N, k0, K, j, lane);
+  };
   auto issue = [&](int kt, bf16_t* st) {
     const int k0 = kt * KT;
 #pragma unroll
-    for (int q = 0; q < NA; ++q) {
-      if constexpr (AK) dma_kc<false>(ga, nullptr, nullptr, 0, m0, k0, K, st, wave, lane, q);
-      else dma_ks<BM>(ga, m0, p.M, k0, K, st, wave, lane, q);
+    for (int q = 0; q < NA; q += 4) {
+      const int n = NA - q >= 4 ? 4 : NA - q;
+      if (n == 4) {
+        DmaLoad l[4] = {load_a(k0, wave * NA + q), load_a(k0, wave * NA + q + 1), load_a(k0, wave * NA + q + 2),
+                        load_a(k0, wave * NA + q + 3)};
+        dma16_group<4>(l, st + (wave * NA + q) * 512);
+      } else {
+        DmaLoad l[2] = {load_a(k0, wave * NA + q), load_a(k0, wave * NA + q + 1)};
+        dma16_group<2>(l, st + (wave * NA + q) * 512);
+      }
     }
 #pragma unroll
-    for (int q = 0; q < NB; ++q) {
-      if constexpr (BKC) dma_kc<EPI == EPI_GLU_FWD>(gb, gate, up, p.glu_rows, n0, k0, K, st + TILE_ELEMS, wave, lane, q);
-      else dma_ks<BN>(gb, n0, p.N, k0, K, st + TILE_ELEMS, wave, lane, q);
+    for (int q = 0; q < NB; q += 4) {
+      const int n = NB - q >= 4 ? 4 : NB - q;
+      if (n == 4) {
+        DmaLoad l[4] = {load_b(k0, wave * NB + q), load_b(k0, wave * NB + q + 1), load_b(k0, wave * NB + q + 2),
+                        load_b(k0, wave * NB + q + 3)};
+        dma16_group<4>(l, st + TILE_ELEMS + (wave * NB + q) * 512);
+      } else {
+        DmaLoad l[2] = {load_b(k0, wave * NB + q), load_b(k0, wave * NB + q + 1)};
+        dma16_group<2>(l, st + TILE_ELEMS + (wave * NB + q) * 512);
+      }
     }
   };
 
