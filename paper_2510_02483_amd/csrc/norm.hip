@@ -10,8 +10,10 @@ namespace ls {
 
 namespace {
 
-constexpr int NORM_WAVES = 4;          // waves per workgroup (one row per wave at a time)
+constexpr int NORM_WAVES = 4;           // forward: waves per workgroup, one row per wave
+constexpr int BWD_WAVES = 8;            // backward: waves per workgroup, two rows per wave at a time
 constexpr int BWD_ROWS_PER_BLOCK = 32;  // rows whose gain gradient one workgroup sums
+constexpr int SUM_GROUPS = 8;           // column sum: part groups per workgroup
 
 LS_DEV void unpack8(const u32x4 w, float f[8]) {
 #pragma unroll
@@ -65,41 +67,51 @@ __global__ __launch_bounds__(64 * NORM_WAVES) void rmsnorm_fwd_kernel(int64_t ro
 
 // dx = dres + r*a - x*r^3*<a,x>/hidden with a = gamma*dh; per-workgroup
 // partial sums of dh*x*r over its rows go to partial[blockIdx.x][hidden].
+// Wave w handles rows w, w+8, w+16, w+24 of the workgroup's 32, each with all
+// its loads (x, dh, dres) issued in one phase; gamma is loaded once.
 template <int CH>
-__global__ __launch_bounds__(64 * NORM_WAVES) void rmsnorm_bwd_kernel(int64_t rows, int hidden,
-                                                                      const bf16_t* __restrict__ x,
-                                                                      const bf16_t* __restrict__ gamma,
-                                                                      const float* __restrict__ r,
-                                                                      const bf16_t* __restrict__ dh,
-                                                                      const bf16_t* __restrict__ dres,
-                                                                      bf16_t* __restrict__ dx,
-                                                                      float* __restrict__ partial) {
+__global__ __launch_bounds__(64 * BWD_WAVES) void rmsnorm_bwd_kernel(int64_t rows, int hidden,
+                                                                     const bf16_t* __restrict__ x,
+                                                                     const bf16_t* __restrict__ gamma,
+                                                                     const float* __restrict__ r,
+                                                                     const bf16_t* __restrict__ dh,
+                                                                     const bf16_t* __restrict__ dres,
+                                                                     bf16_t* __restrict__ dx,
+                                                                     float* __restrict__ partial) {
   __shared__ float red[CH * 512];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int chunks = hidden / 8;
+  u32x4 gv[CH];
   float gsum[CH][8];
 #pragma unroll
-  for (int i = 0; i < CH; ++i)
+  for (int i = 0; i < CH; ++i) {
+    const int c = lane + 64 * i;
+    gv[i] = c < chunks ? *(const u32x4*)(gamma + c * 8) : u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
     for (int e = 0; e < 8; ++e) gsum[i][e] = 0.f;
+  }
   const int64_t row_begin = (int64_t)blockIdx.x * BWD_ROWS_PER_BLOCK;
-  for (int rr = wave; rr < BWD_ROWS_PER_BLOCK; rr += NORM_WAVES) {
+#pragma unroll 1
+  for (int rr = wave; rr < BWD_ROWS_PER_BLOCK; rr += BWD_WAVES) {
     const int64_t row = row_begin + rr;
     if (row >= rows) break;
     const float rs = r[row];
-    u32x4 xv[CH], dv[CH];
-    float dot = 0.f;
+    u32x4 xv[CH], dv[CH], rv[CH];
 #pragma unroll
     for (int i = 0; i < CH; ++i) {
       const int c = lane + 64 * i;
-      xv[i] = dv[i] = u32x4{0u, 0u, 0u, 0u};
-      if (c >= chunks) continue;
-      xv[i] = *(const u32x4*)(x + row * hidden + c * 8);
-      dv[i] = *(const u32x4*)(dh + row * hidden + c * 8);
+      const bool in = c < chunks;
+      xv[i] = in ? *(const u32x4*)(x + row * hidden + c * 8) : u32x4{0u, 0u, 0u, 0u};
+      dv[i] = in ? *(const u32x4*)(dh + row * hidden + c * 8) : u32x4{0u, 0u, 0u, 0u};
+      rv[i] = in && dres ? *(const u32x4*)(dres + row * hidden + c * 8) : u32x4{0u, 0u, 0u, 0u};
+    }
+    float dot = 0.f;
+#pragma unroll
+    for (int i = 0; i < CH; ++i) {
       float xf[8], df[8], g[8];
       unpack8(xv[i], xf);
       unpack8(dv[i], df);
-      unpack8(*(const u32x4*)(gamma + c * 8), g);
+      unpack8(gv[i], g);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         dot += g[e] * df[e] * xf[e];
@@ -115,18 +127,15 @@ __global__ __launch_bounds__(64 * NORM_WAVES) void rmsnorm_bwd_kernel(int64_t ro
       float xf[8], df[8], g[8], o[8], rf[8];
       unpack8(xv[i], xf);
       unpack8(dv[i], df);
-      unpack8(*(const u32x4*)(gamma + c * 8), g);
-      if (dres) unpack8(*(const u32x4*)(dres + row * hidden + c * 8), rf);
-      else
-#pragma unroll
-        for (int e = 0; e < 8; ++e) rf[e] = 0.f;
+      unpack8(gv[i], g);
+      unpack8(rv[i], rf);
 #pragma unroll
       for (int e = 0; e < 8; ++e) o[e] = rf[e] + rs * g[e] * df[e] - xf[e] * coef;
       *(u32x4*)(dx + row * hidden + c * 8) = pack8(o);
     }
   }
   // combine the waves' column sums in a fixed order (deterministic)
-  for (int w = 0; w < NORM_WAVES; ++w) {
+  for (int w = 0; w < BWD_WAVES; ++w) {
     if (wave == w) {
 #pragma unroll
       for (int i = 0; i < CH; ++i)
@@ -138,17 +147,31 @@ __global__ __launch_bounds__(64 * NORM_WAVES) void rmsnorm_bwd_kernel(int64_t ro
     }
     __syncthreads();
   }
-  for (int j = threadIdx.x; j < hidden; j += 64 * NORM_WAVES) partial[(int64_t)blockIdx.x * hidden + j] = red[j];
+  for (int j = threadIdx.x; j < hidden; j += 64 * BWD_WAVES) partial[(int64_t)blockIdx.x * hidden + j] = red[j];
 }
 
-// dgamma[j] (+)= sum over parts of partial[p][j], parts summed in order.
-__global__ void column_sum_kernel(int parts, int hidden, const float* __restrict__ partial,
-                                  float* __restrict__ out, int accumulate) {
-  const int j = blockIdx.x * blockDim.x + threadIdx.x;
-  if (j >= hidden) return;
+// dgamma[j] (+)= sum over parts of partial[p][j]: 64 columns per workgroup,
+// SUM_GROUPS groups of threads sum interleaved parts, and the group sums are
+// added in group order (deterministic).
+__global__ __launch_bounds__(64 * SUM_GROUPS) void column_sum_kernel(int parts, int hidden,
+                                                                     const float* __restrict__ partial,
+                                                                     float* __restrict__ out, int accumulate) {
+  __shared__ float red[SUM_GROUPS][64];
+  const int c = threadIdx.x & 63, g = threadIdx.x >> 6;
+  const int j = blockIdx.x * 64 + c;
   float s = 0.f;
-  for (int p = 0; p < parts; ++p) s += partial[(int64_t)p * hidden + j];
-  out[j] = accumulate ? out[j] + s : s;
+  if (j < hidden) {
+#pragma unroll 8
+    for (int p = g; p < parts; p += SUM_GROUPS) s += partial[(int64_t)p * hidden + j];
+  }
+  red[g][c] = s;
+  __syncthreads();
+  if (g == 0 && j < hidden) {
+    float t = red[0][c];
+#pragma unroll
+    for (int k = 1; k < SUM_GROUPS; ++k) t += red[k][c];
+    out[j] = accumulate ? out[j] + t : t;
+  }
 }
 
 __global__ void rope_table_kernel(int seq, int head_dim, double theta, float* __restrict__ cs) {
@@ -185,7 +208,7 @@ hipError_t rmsnorm_bwd(int64_t rows, int hidden, const bf16_t* x, const bf16_t* 
                        float* partial, hipStream_t s) {
   const int ch = (hidden / 8 + 63) / 64;
   const int parts = rmsnorm_bwd_parts(rows);
-  const dim3 grid((unsigned)parts), block(64 * NORM_WAVES);
+  const dim3 grid((unsigned)parts), block(64 * BWD_WAVES);
 #define LS_B(CHV)                                                                                       \
   case CHV:                                                                                             \
     hipLaunchKernelGGL((rmsnorm_bwd_kernel<CHV>), grid, block, 0, s, rows, hidden, x, gamma, r, dh, dres, dx, \
@@ -199,7 +222,7 @@ hipError_t rmsnorm_bwd(int64_t rows, int hidden, const bf16_t* x, const bf16_t* 
 #undef LS_B
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(column_sum_kernel, dim3((hidden + 255) / 256), dim3(256), 0, s, parts, hidden,
+  hipLaunchKernelGGL(column_sum_kernel, dim3((hidden + 63) / 64), dim3(64 * SUM_GROUPS), 0, s, parts, hidden,
                      (const float*)partial, dgamma, accumulate);
   return hipGetLastError();
 }
