@@ -36,6 +36,7 @@
 // of one row: 8-byte bf16 / 16-byte fp32 stores, and the RoPE and SwiGLU
 // partners of a column sit in the same lane.
 #include <atomic>
+#include <type_traits>
 
 #include "common.h"
 #include "kernels.h"
@@ -96,77 +97,82 @@ LS_DEV int ks_off(int kk, int col) {
 
 LS_DEV float silu_f(float g) { return g * __frcp_rn(1.0f + __expf(-g)); }
 
-// One operand: up to three row segments (rows of B may come from three weight
-// matrices).  For a k-contiguous operand the segments split its m/n rows; for a
-// k-strided one they split its k rows.  Segment starts are multiples of 8, so
-// one load instruction (8 rows, or 2 k-rows) never straddles a segment, and the
-// segment, hence the buffer resource, is uniform per instruction.
-// glu (k-contiguous B only): virtual row n is row (n/128)*64 + n%64 of segment
-// (n/64)%2 (gate and up rows interleaved in blocks of 64).
-struct Segs {
-  const bf16_t *b0, *b1, *b2;
-  int s1, s2;  // starts of segments 1 and 2
-  int rows;    // total rows
-  int64_t ld;  // leading dimension in elements
+// ---- operand loads ------------------------------------------------------------
+// Each wave fills NL consecutive 1 KB blocks of an operand tile per k-tile
+// (blocks wave*NL ..).  What does not change along k is computed once before
+// the k loop: the per-lane byte offset of every load for a tile at k = 0
+// (LS_OOB where the lane's row or column lies outside the operand) and the
+// buffer resources.  Per k-tile only a scalar offset moves, and in a tile cut
+// short by the end of K (or of a k segment of B) the lanes past the end read
+// zeros.
+//
+// k-contiguous operand (rows m or n, 128-byte pieces of k): block j holds
+// tile rows 8j .. 8j+7; lane l writes slot l%8 of row 8j + l/8 with that row's
+// logical chunk c = (l%8) ^ kc_swz(row), i.e. k = k0 + 8c.  The chunk only
+// depends on the parity of j.
+// k-strided operand (rows k, columns m or n): block j holds k-rows 2j and
+// 2j+1 of the tile (W/8 chunks each); lane l < 2 W/8 writes slot l % (W/8) of
+// k-row 2j + l / (W/8) with logical chunk slot ^ ks_swz(k-row); the other lanes
+// of a 192-wide tile load zeros into the padding.
+template <int NL>
+struct OpLoads {
+  i32x4 r[4];         // resources of the operand (or of B's current k segment), see rsrc4
+  uint32_t voff[NL];  // per-lane byte offsets of the loads for the tile at k = 0
+  uint32_t kpos[2];   // k-contiguous: 8c for even / odd blocks; k-strided: l / (W/8)
 };
 
-// Resource and first-row index of the segment that holds row `rb` (uniform).
-LS_DEV i32x4 seg_rsrc(const Segs g, int rb, int& seg_start) {
-  const bf16_t* base;
-  int s0, s_end;
-  if (rb >= g.s2) {
-    base = g.b2; s0 = g.s2; s_end = g.rows;
-  } else if (rb >= g.s1) {
-    base = g.b1; s0 = g.s1; s_end = min(g.s2, g.rows);
-  } else {
-    base = g.b0; s0 = 0; s_end = min(g.s1, g.rows);
+LS_DEV int kc_chunk(int j, int lane) { return (lane & 7) ^ kc_swz(8 * j + (lane >> 3)); }
+
+// k-contiguous operand: tile rows of this wave map to rows lrow0 .. of a
+// resource of `lrows` rows at `base` (leading dimension ld elements).
+template <int NL>
+LS_DEV void kc_setup(OpLoads<NL>& o, const void* base, int lrow0, int lrows, int64_t ld, int lane) {
+  rsrc4(o.r, base, clamp_bytes((int64_t)lrows * ld * 2));
+#pragma unroll
+  for (int l = 0; l < NL; ++l) {
+    const int lr = lrow0 + 8 * l + (lane >> 3);
+    o.voff[l] = lr < lrows ? (uint32_t)((int64_t)lr * ld * 2 + 16 * kc_chunk(l, lane)) : OOB;
   }
-  seg_start = s0;
-  return rsrc(base, clamp_bytes((int64_t)(s_end - s0) * g.ld * 2));
+  o.kpos[0] = 8 * kc_chunk(0, lane);
+  o.kpos[1] = 8 * kc_chunk(1, lane);
 }
 
-// The load of 1 KB block j of a 64-k tile of a k-contiguous operand (rows
-// row0 .. row0+255 or +191, k0 .. k0+63): rows 8j .. 8j+7; lane l writes slot
-// l%8 of row 8j + l/8 with that row's logical chunk (l%8) ^ kc_swz(row), so the
-// 8 lanes of a row fetch its whole 128-byte piece.
-template <bool GLU>
-LS_DEV DmaLoad kc_load(const Segs g, const bf16_t* gate, const bf16_t* up, int glu_rows, int row0, int k0, int K,
-                       int j, int lane) {
-  const int rr = 8 * j + (lane >> 3);
-  const int c = (lane & 7) ^ kc_swz(rr);
-  const int k = k0 + 8 * c;
-  const int rb = row0 + 8 * j;  // first row of the instruction (uniform)
-  int lrow0;
-  i32x4 r;
-  if constexpr (GLU) {
-    r = rsrc((rb >> 6) & 1 ? up : gate, clamp_bytes((int64_t)glu_rows * g.ld * 2));
-    lrow0 = (rb >> 7) * 64 + (rb & 63);
-  } else {
-    int s0;
-    r = seg_rsrc(g, rb, s0);
-    lrow0 = rb - s0;
-  }
-  const int lrow = lrow0 + (lane >> 3);
-  return DmaLoad{r, k < K ? (uint32_t)(lrow * g.ld * 2 + k * 2) : OOB};
-}
-
-// The load of 1 KB block j of a 64-k tile of a k-strided operand (k rows k0 ..
-// k0+63, columns col0 .. col0+W-1 of `cols`): k-rows 2j and 2j+1; lane
-// l < 2 W/8 writes slot l % (W/8) of k-row 2j + l / (W/8) with that row's
-// logical chunk slot ^ ks_swz(k-row); the remaining lanes of a 192-wide tile
-// load zeros into the block's padding.  Segment starts are even.
-template <int W>
-LS_DEV DmaLoad ks_load(const Segs g, int col0, int cols, int k0, int K, int j, int lane) {
+// k-strided operand: columns col0 .. col0 + W - 1 of `cols`; the k rows are
+// placed by the scalar offset (and the resource) of each tile.
+template <int NL, int W>
+LS_DEV void ks_setup(OpLoads<NL>& o, int col0, int cols, int64_t ld, int wave, int lane) {
   constexpr int CPR = W / 8;  // chunks per k-row
-  const int half = lane / CPR;  // 0 or 1 (2: padding lanes)
-  const int kb = k0 + 2 * j;    // first k row of the instruction (uniform)
-  int s0;
-  const i32x4 r = seg_rsrc(g, kb, s0);
-  const int c = (lane % CPR) ^ ks_swz<W>(2 * j + half);
-  const int col = col0 + 8 * c;
-  const int lk = kb - s0 + half;
-  const bool ok = half < 2 && kb + half < K && col < cols;
-  return DmaLoad{r, ok ? (uint32_t)(lk * g.ld * 2 + col * 2) : OOB};
+  const int half = lane / CPR;
+#pragma unroll
+  for (int l = 0; l < NL; ++l) {
+    const int kr = 2 * (wave * NL + l) + half;
+    const int col = col0 + 8 * ((lane % CPR) ^ ks_swz<W>(kr));
+    o.voff[l] = half < 2 && col < cols ? (uint32_t)((int64_t)kr * ld * 2 + col * 2) : OOB;
+  }
+  o.kpos[0] = half;
+  o.kpos[1] = half;
+}
+
+// Offset of load l of a tile with `kvalid` valid k values (64 for a whole tile).
+template <bool KC, int NL>
+LS_DEV uint32_t load_off(const OpLoads<NL>& o, int l, int kvalid, int wave) {
+  const bool ok = KC ? (int)o.kpos[l & 1] < kvalid : (int)o.kpos[0] < kvalid - 2 * (wave * NL + l);
+  return ok ? o.voff[l] : OOB;
+}
+
+// Group g (loads 4g .. 4g+3, or the last two) of an operand tile into the LDS
+// blocks starting at byte address m0 (the wave's first block of the stage).
+template <bool KC, int NL>
+LS_DEV void issue_group(const OpLoads<NL>& o, int g, uint32_t soff, int kvalid, uint32_t m0, int wave) {
+  const int first = 4 * g;
+  if (NL - first >= 4) {
+    const uint32_t v[4] = {load_off<KC>(o, first, kvalid, wave), load_off<KC>(o, first + 1, kvalid, wave),
+                           load_off<KC>(o, first + 2, kvalid, wave), load_off<KC>(o, first + 3, kvalid, wave)};
+    dma_group<4>(o.r, v, soff, m0 + 1024u * first);
+  } else {
+    const uint32_t v[2] = {load_off<KC>(o, first, kvalid, wave), load_off<KC>(o, first + 1, kvalid, wave)};
+    dma_group<2>(o.r, v, soff, m0 + 1024u * first);
+  }
 }
 
 // Fragment of a k-contiguous tile: lane gets row `r` (tile-local), k = 16s + 8*(lane/32) .. +7.
@@ -198,6 +204,21 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
   constexpr int WM = BM / 2, WN = BN / 2;  // wave tile
   constexpr int TM = WM / 32, TN = WN / 32;
   constexpr int NA = AK ? BM / 32 : 8, NB = BKC ? BN / 32 : 8;  // load instructions per wave and tile
+  constexpr int GA = (NA + 3) / 4, GB = (NB + 3) / 4;            // load groups per wave and tile
+  constexpr int NMF = TM * TN;                                   // MFMAs per k-step
+  constexpr int NRU = TM + TN;                                   // fragments per k-step
+  // The last k-step of a tile runs BAR_AT MFMAs, then waits for the next
+  // tile's loads and for the other waves, then reads the next tile's first
+  // fragments between its remaining MFMAs.
+  constexpr int BAR_AT = NMF >= 16 ? 2 : 1;
+  static_assert(BAR_AT + NRU <= NMF, "the next tile's first fragments are read within the last k-step");
+  // The first k-step of a tile issues the next tile's load groups, one after
+  // MFMA 1, 1 + DMA_GAP, ... so that consecutive M0 writes are apart.
+  constexpr int DMA_GAP = (NMF - 2) / (GA + GB);
+  static_assert(DMA_GAP >= 1, "room for the load groups in one k-step");
+  constexpr bool KSEG = !BKC;  // a k-strided B may come from up to three buffers along k
+  constexpr bool GLU = EPI == EPI_GLU_FWD;
+  constexpr uint32_t STAGE_BYTES = 2 * TILE_ELEMS * 2;
   // Two LDS stages of [A tile | B tile].  The buffer->LDS loads are inline
   // assembly the compiler does not see, so the stage can be picked at run time.
   __shared__ __attribute__((aligned(1024))) bf16_t lds[2][2 * TILE_ELEMS];
@@ -210,60 +231,67 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
   map_tile(blockIdx.x, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
   const int K = p.K;
-  const int nk = (K + KT - 1) / KT;
 
-  Segs ga, gb;
-  ga.b0 = ga.b1 = ga.b2 = p.A;
-  ga.s1 = ga.s2 = 1 << 30;
-  ga.rows = AK ? p.M : K;
-  ga.ld = p.lda;
-  gb.b0 = p.B[0];
-  gb.b1 = p.B[1] ? p.B[1] : p.B[0];
-  gb.b2 = p.B[2] ? p.B[2] : p.B[0];
-  gb.s1 = p.b_start[1];
-  gb.s2 = p.b_start[2];
-  gb.rows = BKC ? p.N : K;
-  gb.ld = p.ldb;
+  // k segments of B: [0, S1), [S1, S2), [S2, K) (one segment unless a
+  // k-strided B is split over buffers).  The tiles of a segment start at its
+  // first k; the last one may be cut short.
+  int S1 = K, S2 = K;
+  if constexpr (KSEG) {
+    S1 = min(p.b_start[1], K);
+    S2 = max(S1, min(p.b_start[2], K));
+  }
+  auto seg_end = [&](int k) { return k < S1 ? S1 : (k < S2 ? S2 : K); };
+  const int nk = (S1 + KT - 1) / KT + (S2 - S1 + KT - 1) / KT + (K - S2 + KT - 1) / KT;
 
-  const bf16_t* gate = p.B[0];
-  const bf16_t* up = p.B[1];
-  // The loads of tile kt into stage st: wave w fills the NA consecutive 1 KB
-  // blocks w*NA .. of the A tile and the NB blocks w*NB .. of the B tile, in
-  // groups of four (one M0 write per group).
-  auto load_a = [&](int k0, int j) -> DmaLoad {
-    if constexpr (AK) return kc_load<false>(ga, nullptr, nullptr, 0, m0, k0, K, j, lane);
-    else return ks_load<BM>(ga, m0, p.M, k0, K, j, lane);
-  };
-  auto load_b = [&](int k0, int j) -> DmaLoad {
-    if constexpr (BKC) return kc_load<EPI == EPI_GLU_FWD>(gb, gate, up, p.glu_rows, n0, k0, K, j, lane);
-    else return ks_load<BN>(gb, n0, p.N, k0, K, j, lane);
-  };
-  auto issue = [&](int kt, bf16_t* st) {
-    const int k0 = kt * KT;
-#pragma unroll
-    for (int q = 0; q < NA; q += 4) {
-      const int n = NA - q >= 4 ? 4 : NA - q;
-      if (n == 4) {
-        DmaLoad l[4] = {load_a(k0, wave * NA + q), load_a(k0, wave * NA + q + 1), load_a(k0, wave * NA + q + 2),
-                        load_a(k0, wave * NA + q + 3)};
-        dma16_group<4>(l, st + (wave * NA + q) * 512);
-      } else {
-        DmaLoad l[2] = {load_a(k0, wave * NA + q), load_a(k0, wave * NA + q + 1)};
-        dma16_group<2>(l, st + (wave * NA + q) * 512);
-      }
+  OpLoads<NA> la;
+  OpLoads<NB> lb;
+  if constexpr (AK) {
+    kc_setup(la, p.A, m0 + wave * NA * 8, p.M, p.lda, lane);
+  } else {
+    ks_setup<NA, BM>(la, m0, p.M, p.lda, wave, lane);
+    rsrc4(la.r, p.A, clamp_bytes((int64_t)K * p.lda * 2));
+  }
+  if constexpr (BKC) {
+    const int rb = n0 + wave * NB * 8;  // first row of the wave's blocks (uniform)
+    if constexpr (GLU) {
+      // gate and up rows interleaved in blocks of 64: a wave's 64 rows are one block
+      kc_setup(lb, (rb >> 6) & 1 ? p.B[1] : p.B[0], (rb >> 7) * 64, p.glu_rows, p.ldb, lane);
+    } else {
+      // row segments start at multiples of 64, so a wave's 64 rows lie in one
+      const int sg = rb >= p.b_start[2] ? 2 : (rb >= p.b_start[1] ? 1 : 0);
+      const int st = sg == 2 ? p.b_start[2] : (sg == 1 ? p.b_start[1] : 0);
+      const int en = min(p.N, sg == 2 ? p.N : (sg == 1 ? p.b_start[2] : p.b_start[1]));
+      kc_setup(lb, p.B[sg], rb - st, en - st, p.ldb, lane);
     }
-#pragma unroll
-    for (int q = 0; q < NB; q += 4) {
-      const int n = NB - q >= 4 ? 4 : NB - q;
-      if (n == 4) {
-        DmaLoad l[4] = {load_b(k0, wave * NB + q), load_b(k0, wave * NB + q + 1), load_b(k0, wave * NB + q + 2),
-                        load_b(k0, wave * NB + q + 3)};
-        dma16_group<4>(l, st + TILE_ELEMS + (wave * NB + q) * 512);
-      } else {
-        DmaLoad l[2] = {load_b(k0, wave * NB + q), load_b(k0, wave * NB + q + 1)};
-        dma16_group<2>(l, st + TILE_ELEMS + (wave * NB + q) * 512);
-      }
+  } else {
+    ks_setup<NB, BN>(lb, n0, p.N, p.ldb, wave, lane);
+    if constexpr (!KSEG) rsrc4(lb.r, p.B[0], clamp_bytes((int64_t)K * p.ldb * 2));
+  }
+
+  // The load cursor: first k of the next tile to load, its valid k count and
+  // the scalar offsets of both operands (B's resource follows its segment).
+  int ck = 0, kval = 0;
+  uint32_t soa = 0, sob = 0;
+  auto set_cursor = [&](int k0) {
+    ck = k0;
+    const int se = seg_end(k0);
+    kval = min(KT, se - k0);
+    soa = AK ? (uint32_t)(k0 * 2) : (uint32_t)((int64_t)k0 * p.lda * 2);
+    if constexpr (KSEG) {
+      const int sg = k0 >= S2 ? 2 : (k0 >= S1 ? 1 : 0);
+      const int st = sg == 2 ? S2 : (sg == 1 ? S1 : 0);
+      const bf16_t* bp = p.B[sg] ? p.B[sg] : p.B[0];
+      rsrc4(lb.r, bp, clamp_bytes((int64_t)(se - st) * p.ldb * 2));
+      sob = (uint32_t)((int64_t)(k0 - st) * p.ldb * 2);
+    } else {
+      sob = BKC ? (uint32_t)(k0 * 2) : (uint32_t)((int64_t)k0 * p.ldb * 2);
     }
+  };
+  const uint32_t lds0 = lds_offset(&lds[0][0]);
+  const uint32_t ma = lds0 + wave * NA * 1024, mb = lds0 + TILE_ELEMS * 2 + wave * NB * 1024;
+  auto issue = [&](int g, uint32_t stage_off) {
+    if (g < GA) issue_group<AK, NA>(la, g, soa, kval, ma + stage_off, wave);
+    else issue_group<BKC, NB>(lb, g - GA, sob, kval, mb + stage_off, wave);
   };
 
   f32x16 acc[TM][TN];
@@ -275,54 +303,63 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
   const int lr = lane & 31, lh = lane >> 5;
-
-  // The k loop is one continuous stream of 16-k steps (four per 64-k tile):
-  // while the matrix cores work on one step, the fragments of the next step
-  // are read from LDS, across tile boundaries too.  At the start of tile kk
-  // the other stage (tile kk-1) is free, and the loads of tile kk+1 go there;
-  // before the last step of tile kk every wave waits for its own loads of tile
-  // kk+1 (vmcnt) and then for the other waves (barrier), and only then reads
-  // the first fragments of tile kk+1.  The same barrier tells every wave that
-  // all reads of tile kk are done before tile kk+2 overwrites its stage.
   u32x4 af[2][TM], bfr[2][TN];
-  auto load_frags = [&](int stage, int s, int buf) {
+  // Fragment u of a k-step: A fragments 0 .. TM-1, then B fragments.
+  auto read_unit = [&](int stage, int s, int buf, int u) {
     const bf16_t* as = lds[stage];
     const bf16_t* bs = lds[stage] + TILE_ELEMS;
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-      af[buf][i] = AK ? frag_kc(as, wm * WM + 32 * i + lr, s, lh) : frag_ks<BM>(as, wm * WM + 32 * i, s, lane);
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-      bfr[buf][j] = BKC ? frag_kc(bs, wn * WN + 32 * j + lr, s, lh) : frag_ks<BN>(bs, wn * WN + 32 * j, s, lane);
+    if (u < TM) {
+      af[buf][u] = AK ? frag_kc(as, wm * WM + 32 * u + lr, s, lh) : frag_ks<BM>(as, wm * WM + 32 * u, s, lane);
+    } else {
+      const int v = u - TM;
+      bfr[buf][v] = BKC ? frag_kc(bs, wn * WN + 32 * v + lr, s, lh) : frag_ks<BN>(bs, wn * WN + 32 * v, s, lane);
+    }
   };
-  auto mfmas = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j) acc[i][j] = mfma32(bfr[buf][j], af[buf][i], acc[i][j]);
-  };
-  auto sync_tile = []() { sync_lds(); };
 
-  issue(0, lds[0]);
-  sync_tile();
-  load_frags(0, 0, 0);
-  for (int kk = 0; kk < nk; ++kk) {
-    const int cur = kk & 1;
-    if (kk + 1 < nk) issue(kk + 1, lds[cur ^ 1]);
+  // One 64-k tile in stage `cur`.  The k loop is one continuous stream of
+  // 16-k steps: the fragments of step s+1 are read between the MFMAs of step
+  // s, across tile boundaries too.  The first step issues the loads of the
+  // next tile into the other stage (free since the barrier of the previous
+  // tile); the last step waits for them (vmcnt) and for the other waves
+  // (barrier), and only then reads the next tile's first fragments.  The same
+  // barrier tells every wave that the reads of this stage are done before the
+  // loads of the tile after next overwrite it.  Every instruction is pinned in
+  // place with scheduling barriers.
+  auto tile = [&](auto has_next, int cur) {
+    constexpr bool HN = decltype(has_next)::value;
+    const uint32_t nxt = (uint32_t)(cur ^ 1) * STAGE_BYTES;
 #pragma unroll
     for (int s = 0; s < KSTEPS; ++s) {
       const int buf = s & 1;
-      __builtin_amdgcn_sched_barrier(0);
-      if (s + 1 < KSTEPS) {
-        load_frags(cur, s + 1, buf ^ 1);
-      } else if (kk + 1 < nk) {
-        sync_tile();
-        load_frags(cur ^ 1, 0, buf ^ 1);
+#pragma unroll
+      for (int i = 0; i < NMF; ++i) {
+        if (HN && s == KSTEPS - 1 && i == BAR_AT) sync_lds();
+        __builtin_amdgcn_sched_barrier(0);
+        acc[i / TN][i % TN] = mfma32(bfr[buf][i % TN], af[buf][i / TN], acc[i / TN][i % TN]);
+        if (s + 1 < KSTEPS) {
+          if (i < NRU) read_unit(cur, s + 1, buf ^ 1, i);
+        } else if (HN) {
+          if (i >= BAR_AT && i < BAR_AT + NRU) read_unit(cur ^ 1, 0, buf ^ 1, i - BAR_AT);
+        }
+        if (HN && s == 0 && i >= 1 && (i - 1) % DMA_GAP == 0 && (i - 1) / DMA_GAP < GA + GB) {
+          issue((i - 1) / DMA_GAP, nxt);
+          if ((i - 1) / DMA_GAP == GA + GB - 1) set_cursor(ck + kval);
+        }
+        __builtin_amdgcn_sched_barrier(0);
       }
-      __builtin_amdgcn_sched_barrier(0);
-      mfmas(buf);
     }
-  }
+  };
+
+  set_cursor(0);
+#pragma unroll
+  for (int g = 0; g < GA + GB; ++g) issue(g, 0);
+  set_cursor(ck + kval);
+  sync_lds();
+#pragma unroll
+  for (int u = 0; u < NRU; ++u) read_unit(0, 0, 0, u);
+  for (int kt = 0; kt + 1 < nk; ++kt) tile(std::true_type{}, kt & 1);
+  tile(std::false_type{}, (nk - 1) & 1);
+  auto sync_tile = []() { sync_lds(); };
   sync_tile();  // every wave is done with both stages before they become staging space
 
   // ---- epilogue ---------------------------------------------------------------
@@ -596,6 +633,10 @@ int gemm_tile_override(int bm, int bn) {
 }
 
 hipError_t gemm(const GemmArgs& a, hipStream_t s) {
+  // A k-contiguous B split over buffers (or gate/up interleaved) is loaded a
+  // wave's 64 rows at a time from one buffer: segments start at multiples of 64.
+  if (a.b_kcontig && ((a.b_start[1] % 64 && a.b_start[1] < a.N) || (a.b_start[2] % 64 && a.b_start[2] < a.N)))
+    return hipErrorInvalidValue;
   if (a.a_kcontig && a.b_kcontig) {
     switch (a.epi) {
       case EPI_BF16:
