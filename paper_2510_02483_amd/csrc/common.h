@@ -131,43 +131,20 @@ LS_DEV void dma16_group(DmaLoad (&l)[N], const void* lds) {
   }
 }
 
-// The four resources of a group of up to four buffer->LDS loads over
-// [base, base + bytes): load i of a group carries the instruction offset i KB,
-// which moves its LDS address and its memory address alike, so its resource
-// starts i KB earlier (and is i KB longer) to read the same bytes.
-LS_DEV void rsrc4(i32x4 (&r)[4], const void* base, uint32_t bytes) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i) r[i] = rsrc((const char*)base - 1024 * i, bytes + 1024u * i);
+// One buffer->LDS load with a scalar offset: 16 bytes per lane from offset
+// soff + voff of the buffer (zero outside it) into LDS at m0 + 16 lane.  The
+// scalar offset moves every load of a tile along k; voff = LS_OOB reads zeros.
+// The M0 write waits until the wave's earlier loads have left the issue
+// stage, so callers keep other instructions between consecutive loads.
+LS_DEV void dma1(i32x4 r, uint32_t voff, uint32_t soff, uint32_t m0) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+               :
+               : "s"(m0), "v"(voff), "s"(r), "s"(soff)
+               : "memory", "m0");
 }
 
-// N (2 or 4) buffer->LDS loads with one M0 write: load i reads offset
-// soff + v[i] of resource r[i] (see rsrc4) into the 1 KB LDS block at
-// m0 + i KB, 16 bytes per lane.  The scalar offset soff moves every load of
-// a tile along k; an offset v[i] of LS_OOB reads zeros.
-template <int N>
-LS_DEV void dma_group(const i32x4 (&r)[4], const uint32_t (&v)[N], uint32_t soff, uint32_t m0) {
-  if constexpr (N == 4) {
-    asm volatile(
-        "s_mov_b32 m0, %0\n\ts_nop 0\n\t"
-        "buffer_load_dwordx4 %1, %5, %9 offen lds\n\t"
-        "buffer_load_dwordx4 %2, %6, %9 offen offset:1024 lds\n\t"
-        "buffer_load_dwordx4 %3, %7, %9 offen offset:2048 lds\n\t"
-        "buffer_load_dwordx4 %4, %8, %9 offen offset:3072 lds"
-        :
-        : "s"(m0), "v"(v[0]), "v"(v[1]), "v"(v[2]), "v"(v[3]), "s"(r[0]), "s"(r[1]), "s"(r[2]), "s"(r[3]),
-          "s"(soff)
-        : "memory", "m0");
-  } else {
-    static_assert(N == 2, "groups of 2 or 4 loads");
-    asm volatile(
-        "s_mov_b32 m0, %0\n\ts_nop 0\n\t"
-        "buffer_load_dwordx4 %1, %3, %5 offen lds\n\t"
-        "buffer_load_dwordx4 %2, %4, %5 offen offset:1024 lds"
-        :
-        : "s"(m0), "v"(v[0]), "v"(v[1]), "s"(r[0]), "s"(r[1]), "s"(soff)
-        : "memory", "m0");
-  }
-}
+// s_waitcnt for at most n (0..63) outstanding vector-memory operations.
+#define LS_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | 0x0f70)
 
 // Wait for every buffer->LDS load of this wave and every LDS access, then for
 // the whole workgroup.  A plain s_barrier: __syncthreads() does not know about

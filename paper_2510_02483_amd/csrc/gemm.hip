@@ -53,7 +53,25 @@ constexpr int TILE_ELEMS = 256 * KT;        // LDS region of one operand tile (3
 constexpr int GROUP_M = 8;                  // tile rows per group in the launch order
 constexpr int EPI_ROPE64 = 100;             // EPI_ROPE for 64-wide heads
 constexpr uint32_t OOB = LS_OOB;
+#ifndef GEMM_LOAD_SPAN_PCT
+#define GEMM_LOAD_SPAN_PCT 60  // share of a tile's MFMA slots over which its loads are spread
+#endif
+#ifndef GEMM_READ_AHEAD
+#define GEMM_READ_AHEAD 2  // k-steps between a fragment read and its MFMAs
+#endif
 
+
+// f(integral_constant<int, 0>), ..., f(integral_constant<int, N-1>): a loop
+// unrolled at compile time, so that indices into register arrays and the
+// schedule of every slot are constants whatever the size of the body.
+template <class F, int... I>
+LS_DEV void static_for_(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, class F>
+LS_DEV void static_for(F&& f) {
+  static_for_(f, std::make_integer_sequence<int, N>{});
+}
 
 // Launch order: workgroups are handed to the 8 XCDs round-robin, so first
 // renumber them so that each XCD receives a contiguous range of logical tiles,
@@ -116,7 +134,7 @@ LS_DEV float silu_f(float g) { return g * __frcp_rn(1.0f + __expf(-g)); }
 // of a 192-wide tile load zeros into the padding.
 template <int NL>
 struct OpLoads {
-  i32x4 r[4];         // resources of the operand (or of B's current k segment), see rsrc4
+  i32x4 r;            // resource of the operand (or of B's current k segment)
   uint32_t voff[NL];  // per-lane byte offsets of the loads for the tile at k = 0
   uint32_t kpos[2];   // k-contiguous: 8c for even / odd blocks; k-strided: l / (W/8)
 };
@@ -127,7 +145,7 @@ LS_DEV int kc_chunk(int j, int lane) { return (lane & 7) ^ kc_swz(8 * j + (lane 
 // resource of `lrows` rows at `base` (leading dimension ld elements).
 template <int NL>
 LS_DEV void kc_setup(OpLoads<NL>& o, const void* base, int lrow0, int lrows, int64_t ld, int lane) {
-  rsrc4(o.r, base, clamp_bytes((int64_t)lrows * ld * 2));
+  o.r = rsrc(base, clamp_bytes((int64_t)lrows * ld * 2));
 #pragma unroll
   for (int l = 0; l < NL; ++l) {
     const int lr = lrow0 + 8 * l + (lane >> 3);
@@ -160,19 +178,11 @@ LS_DEV uint32_t load_off(const OpLoads<NL>& o, int l, int kvalid, int wave) {
   return ok ? o.voff[l] : OOB;
 }
 
-// Group g (loads 4g .. 4g+3, or the last two) of an operand tile into the LDS
-// blocks starting at byte address m0 (the wave's first block of the stage).
+// Load l of an operand tile into the LDS block at byte address m0 + l KB
+// (m0: the wave's first block of the stage).
 template <bool KC, int NL>
-LS_DEV void issue_group(const OpLoads<NL>& o, int g, uint32_t soff, int kvalid, uint32_t m0, int wave) {
-  const int first = 4 * g;
-  if (NL - first >= 4) {
-    const uint32_t v[4] = {load_off<KC>(o, first, kvalid, wave), load_off<KC>(o, first + 1, kvalid, wave),
-                           load_off<KC>(o, first + 2, kvalid, wave), load_off<KC>(o, first + 3, kvalid, wave)};
-    dma_group<4>(o.r, v, soff, m0 + 1024u * first);
-  } else {
-    const uint32_t v[2] = {load_off<KC>(o, first, kvalid, wave), load_off<KC>(o, first + 1, kvalid, wave)};
-    dma_group<2>(o.r, v, soff, m0 + 1024u * first);
-  }
+LS_DEV void load_one(const OpLoads<NL>& o, int l, uint32_t soff, int kvalid, uint32_t m0, int wave) {
+  dma1(o.r, load_off<KC>(o, l, kvalid, wave), soff, m0 + 1024u * l);
 }
 
 // Fragment of a k-contiguous tile: lane gets row `r` (tile-local), k = 16s + 8*(lane/32) .. +7.
@@ -204,18 +214,29 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
   constexpr int WM = BM / 2, WN = BN / 2;  // wave tile
   constexpr int TM = WM / 32, TN = WN / 32;
   constexpr int NA = AK ? BM / 32 : 8, NB = BKC ? BN / 32 : 8;  // load instructions per wave and tile
-  constexpr int GA = (NA + 3) / 4, GB = (NB + 3) / 4;            // load groups per wave and tile
+  constexpr int NL = NA + NB;                                    // loads per wave and tile
   constexpr int NMF = TM * TN;                                   // MFMAs per k-step
   constexpr int NRU = TM + TN;                                   // fragments per k-step
   // The last k-step of a tile runs BAR_AT MFMAs, then waits for the next
   // tile's loads and for the other waves, then reads the next tile's first
-  // fragments between its remaining MFMAs.
+  // fragments between its remaining MFMAs.  From the same point on, the
+  // loads of the tile after next go into the stage this tile has just
+  // released, spread evenly over the next LSPAN MFMA slots (into the next
+  // tile): issued back to back, the four waves' loads outrun the rate at which
+  // the texture units take buffer->LDS loads, and a wave whose load does not
+  // fit into the full address queue stalls its matrix core.  The rest of the
+  // period is left for the last loads to arrive.
   constexpr int BAR_AT = NMF >= 16 ? 2 : 1;
-  static_assert(BAR_AT + NRU <= NMF, "the next tile's first fragments are read within the last k-step");
-  // The first k-step of a tile issues the next tile's load groups, one after
-  // MFMA 1, 1 + DMA_GAP, ... so that consecutive M0 writes are apart.
-  constexpr int DMA_GAP = (NMF - 2) / (GA + GB);
-  static_assert(DMA_GAP >= 1, "room for the load groups in one k-step");
+  static_assert(BAR_AT + NRU <= NMF, "the next tile's first fragments are read within one k-step");
+  constexpr int LSPAN = (KSTEPS * NMF * GEMM_LOAD_SPAN_PCT) / 100;
+  static_assert(BAR_AT + LSPAN < KSTEPS * NMF, "every load is issued before the next barrier");
+  // Fragments are read RA k-steps ahead of the MFMAs that use them (RA + 1
+  // register buffers; with RA = 2 four, one per k-step of a tile), so that a
+  // read delayed by the buffer->LDS writes does not hold up the matrix core.
+  constexpr int RA = GEMM_READ_AHEAD;
+  static_assert(RA == 1 || RA == 2, "read-ahead of one or two k-steps");
+  constexpr int NBUF = RA == 1 ? 2 : 4;
+  constexpr int BS = KSTEPS - RA;  // the k-step of a tile that holds the barrier
   constexpr bool KSEG = !BKC;  // a k-strided B may come from up to three buffers along k
   constexpr bool GLU = EPI == EPI_GLU_FWD;
   constexpr uint32_t STAGE_BYTES = 2 * TILE_ELEMS * 2;
@@ -249,7 +270,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
     kc_setup(la, p.A, m0 + wave * NA * 8, p.M, p.lda, lane);
   } else {
     ks_setup<NA, BM>(la, m0, p.M, p.lda, wave, lane);
-    rsrc4(la.r, p.A, clamp_bytes((int64_t)K * p.lda * 2));
+    la.r = rsrc(p.A, clamp_bytes((int64_t)K * p.lda * 2));
   }
   if constexpr (BKC) {
     const int rb = n0 + wave * NB * 8;  // first row of the wave's blocks (uniform)
@@ -265,7 +286,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
     }
   } else {
     ks_setup<NB, BN>(lb, n0, p.N, p.ldb, wave, lane);
-    if constexpr (!KSEG) rsrc4(lb.r, p.B[0], clamp_bytes((int64_t)K * p.ldb * 2));
+    if constexpr (!KSEG) lb.r = rsrc(p.B[0], clamp_bytes((int64_t)K * p.ldb * 2));
   }
 
   // The load cursor: first k of the next tile to load, its valid k count and
@@ -281,7 +302,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
       const int sg = k0 >= S2 ? 2 : (k0 >= S1 ? 1 : 0);
       const int st = sg == 2 ? S2 : (sg == 1 ? S1 : 0);
       const bf16_t* bp = p.B[sg] ? p.B[sg] : p.B[0];
-      rsrc4(lb.r, bp, clamp_bytes((int64_t)(se - st) * p.ldb * 2));
+      lb.r = rsrc(bp, clamp_bytes((int64_t)(se - st) * p.ldb * 2));
       sob = (uint32_t)((int64_t)(k0 - st) * p.ldb * 2);
     } else {
       sob = BKC ? (uint32_t)(k0 * 2) : (uint32_t)((int64_t)k0 * p.ldb * 2);
@@ -289,9 +310,10 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
   };
   const uint32_t lds0 = lds_offset(&lds[0][0]);
   const uint32_t ma = lds0 + wave * NA * 1024, mb = lds0 + TILE_ELEMS * 2 + wave * NB * 1024;
-  auto issue = [&](int g, uint32_t stage_off) {
-    if (g < GA) issue_group<AK, NA>(la, g, soa, kval, ma + stage_off, wave);
-    else issue_group<BKC, NB>(lb, g - GA, sob, kval, mb + stage_off, wave);
+  // Load q of the tile at the cursor (A loads first) into the stage at byte offset stage_off.
+  auto issue = [&](int q, uint32_t stage_off) {
+    if (q < NA) load_one<AK, NA>(la, q, soa, kval, ma + stage_off, wave);
+    else load_one<BKC, NB>(lb, q - NA, sob, kval, mb + stage_off, wave);
   };
 
   f32x16 acc[TM][TN];
@@ -303,7 +325,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
   const int lr = lane & 31, lh = lane >> 5;
-  u32x4 af[2][TM], bfr[2][TN];
+  u32x4 af[NBUF][TM], bfr[NBUF][TN];
   // Fragment u of a k-step: A fragments 0 .. TM-1, then B fragments.
   auto read_unit = [&](int stage, int s, int buf, int u) {
     const bf16_t* as = lds[stage];
@@ -316,49 +338,85 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
     }
   };
 
-  // One 64-k tile in stage `cur`.  The k loop is one continuous stream of
-  // 16-k steps: the fragments of step s+1 are read between the MFMAs of step
-  // s, across tile boundaries too.  The first step issues the loads of the
-  // next tile into the other stage (free since the barrier of the previous
-  // tile); the last step waits for them (vmcnt) and for the other waves
-  // (barrier), and only then reads the next tile's first fragments.  The same
-  // barrier tells every wave that the reads of this stage are done before the
-  // loads of the tile after next overwrite it.  Every instruction is pinned in
-  // place with scheduling barriers.
-  auto tile = [&](auto has_next, int cur) {
-    constexpr bool HN = decltype(has_next)::value;
-    const uint32_t nxt = (uint32_t)(cur ^ 1) * STAGE_BYTES;
-#pragma unroll
-    for (int s = 0; s < KSTEPS; ++s) {
-      const int buf = s & 1;
-#pragma unroll
-      for (int i = 0; i < NMF; ++i) {
-        if (HN && s == KSTEPS - 1 && i == BAR_AT) sync_lds();
+  // MFMA slot (counted from the start of the barrier's k-step) of load q of
+  // the tile after next.
+  constexpr auto slot_of = [](int q) { return BAR_AT + (q * LSPAN) / NL; };
+  constexpr auto bufi = [](int s) { return NBUF == 4 ? s : s & 1; };
+
+  // One 64-k tile in stage `cur` (NX: how many of the next two tiles exist).
+  // The k loop is one continuous stream of 16-k steps: the fragments of step
+  // s+RA are read between the MFMAs of step s, across tile boundaries too.  In
+  // k-step BS each wave waits for its loads of the next tile (vmcnt) and for
+  // the other waves (barrier): then the next tile is in LDS and every wave is
+  // done reading this stage (its last fragments were read one step earlier),
+  // so the loads of the tile after next can go into it while the MFMAs run.
+  // Every instruction is pinned in place with scheduling barriers.
+  auto tile = [&](auto nx_c, int cur) {
+    constexpr int NX = decltype(nx_c)::value;
+    const uint32_t here = (uint32_t)cur * STAGE_BYTES, there = (uint32_t)(cur ^ 1) * STAGE_BYTES;
+    static_for<KSTEPS>([&](auto s_c) {
+      constexpr int s = s_c;
+      constexpr int buf = bufi(s);
+      constexpr int t = s + RA;  // step whose fragments are read now (>= KSTEPS: the next tile's)
+      static_for<NMF>([&](auto i_c) {
+        constexpr int i = i_c;
+        if constexpr (NX >= 1 && s == BS && i == BAR_AT) sync_lds();
         __builtin_amdgcn_sched_barrier(0);
         acc[i / TN][i % TN] = mfma32(bfr[buf][i % TN], af[buf][i / TN], acc[i / TN][i % TN]);
-        if (s + 1 < KSTEPS) {
-          if (i < NRU) read_unit(cur, s + 1, buf ^ 1, i);
-        } else if (HN) {
-          if (i >= BAR_AT && i < BAR_AT + NRU) read_unit(cur ^ 1, 0, buf ^ 1, i - BAR_AT);
+        if constexpr (t < KSTEPS) {
+          if constexpr (i < NRU) read_unit(cur, t, bufi(t), i);
+        } else if constexpr (NX >= 1) {
+          constexpr int u = s == BS ? i - BAR_AT : i;
+          if constexpr (u >= 0 && u < NRU) read_unit(cur ^ 1, t - KSTEPS, bufi(t - KSTEPS), u);
         }
-        if (HN && s == 0 && i >= 1 && (i - 1) % DMA_GAP == 0 && (i - 1) / DMA_GAP < GA + GB) {
-          issue((i - 1) / DMA_GAP, nxt);
-          if ((i - 1) / DMA_GAP == GA + GB - 1) set_cursor(ck + kval);
-        }
+        static_for<NL>([&](auto q_c) {
+          constexpr int q = q_c;
+          constexpr int at = slot_of(q) + BS * NMF;  // tile-relative slot of load q (may be in the next tile)
+          // the later loads of the next tile (its first ones went out in the previous tile)
+          if constexpr (NX >= 1 && at >= KSTEPS * NMF && at - KSTEPS * NMF == s * NMF + i) {
+            issue(q, there);
+            if constexpr (q == NL - 1) set_cursor(ck + kval);
+          }
+          // the first loads of the tile after next, into this stage
+          if constexpr (NX >= 2 && at < KSTEPS * NMF && at == s * NMF + i) {
+            issue(q, here);
+            if constexpr (q == NL - 1) set_cursor(ck + kval);
+          }
+        });
         __builtin_amdgcn_sched_barrier(0);
-      }
-    }
+      });
+    });
   };
 
+  // Prologue: tile 0 whole, then the loads of tile 1 that the previous tile
+  // would have issued in its last k-step; wait for tile 0.
+  constexpr int FIRST = [] {
+    int n = 0;
+    for (int q = 0; q < NL; ++q) n += BAR_AT + (q * LSPAN) / NL + BS * NMF < KSTEPS * NMF;
+    return n;
+  }();
   set_cursor(0);
 #pragma unroll
-  for (int g = 0; g < GA + GB; ++g) issue(g, 0);
+  for (int q = 0; q < NL; ++q) issue(q, 0);
   set_cursor(ck + kval);
-  sync_lds();
+  if (nk > 1) {
 #pragma unroll
-  for (int u = 0; u < NRU; ++u) read_unit(0, 0, 0, u);
-  for (int kt = 0; kt + 1 < nk; ++kt) tile(std::true_type{}, kt & 1);
-  tile(std::false_type{}, (nk - 1) & 1);
+    for (int q = 0; q < FIRST; ++q) issue(q, STAGE_BYTES);
+    if (FIRST == NL) set_cursor(ck + kval);
+    LS_WAIT_VMCNT(FIRST);
+  } else {
+    LS_WAIT_VMCNT(0);
+  }
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+#pragma unroll
+  for (int t = 0; t < RA; ++t)
+#pragma unroll
+    for (int u = 0; u < NRU; ++u) read_unit(0, t, bufi(t), u);
+  int kt = 0;
+  for (; kt + 2 < nk; ++kt) tile(std::integral_constant<int, 2>{}, kt & 1);
+  if (kt + 1 < nk) tile(std::integral_constant<int, 1>{}, kt++ & 1);
+  tile(std::integral_constant<int, 0>{}, kt & 1);
   auto sync_tile = []() { sync_lds(); };
   sync_tile();  // every wave is done with both stages before they become staging space
 
