@@ -28,6 +28,11 @@ CFLAGS = [
     "-Wno-unused-command-line-argument",
 ]
 
+# The attention kernels keep their matrix-product accumulators in ordinary
+# vector registers (the softmax works on them), which leaves the accumulation
+# registers free for values that only the matrix cores read.
+EXTRA = {"attention.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+
 
 def build(verbose: bool = False) -> str:
     """Compile every source and link libls.so next to this file; returns its path."""
@@ -37,7 +42,7 @@ def build(verbose: bool = False) -> str:
         for src in SOURCES:
             obj = os.path.join(tmp, src + ".o")
             objs.append(obj)
-            cmd = [HIPCC, *CFLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+            cmd = [HIPCC, *CFLAGS, *EXTRA.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
             if verbose:
                 print(" ".join(cmd), flush=True)
             procs.append((src, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)))

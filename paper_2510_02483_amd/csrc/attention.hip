@@ -85,6 +85,11 @@ template <int D, int ROWS>
 LS_DEV void load_tile(i32x4 r, int64_t ld, int row0, int rows, int col0, bf16_t* t, int wave, int lane) {
   constexpr int CPR = D / 8, RPI = 64 / CPR, NI = ROWS / RPI, PER = NI / 4;
   static_assert(NI % 4 == 0 && (PER == 2 || PER == 4), "loads split evenly over 4 waves in groups of 2 or 4");
+  // The per-lane offsets are recomputed at every call from the lane index
+  // (itself recomputed here) rather than hoisted out of the tile loop, where
+  // they would hold registers for the whole loop.
+  (void)lane;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(lane));
   DmaLoad l[PER];
 #pragma unroll
   for (int jj = 0; jj < PER; ++jj) {
@@ -92,7 +97,9 @@ LS_DEV void load_tile(i32x4 r, int64_t ld, int row0, int rows, int col0, bf16_t*
     const int rr = j * RPI + lane / CPR;
     const int c = (lane % CPR) ^ tile_swz<D>(rr);
     const int gr = row0 + rr;
-    l[jj] = DmaLoad{r, gr < rows ? (uint32_t)(((int64_t)gr * ld + col0 + 8 * c) * 2) : LS_OOB};
+    // 32-bit offsets: every buffer is below 2 GiB
+    const uint32_t off = ((uint32_t)gr * (uint32_t)ld + (uint32_t)(col0 + 8 * c)) * 2u;
+    l[jj] = DmaLoad{r, gr < rows ? off : LS_OOB};
   }
   dma16_group<PER>(l, t + wave * PER * 512);
 }
@@ -253,10 +260,13 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnShape sh, const bf
   }
 }
 
-// D[b,h,s] = <dO, O> over the head's d columns (fp32).
+// D[b,h,s] = <dO, O> over the head's d columns (fp32), and the log-sum-exp in
+// base 2 (lse * log2(e)), the form the backward kernels subtract.
 template <int D>
 __global__ __launch_bounds__(256) void attn_bwd_pre_kernel(AttnShape sh, const bf16_t* __restrict__ o,
-                                                           const bf16_t* __restrict__ dout, float* __restrict__ Dv) {
+                                                           const bf16_t* __restrict__ dout,
+                                                           const float* __restrict__ lse, float* __restrict__ Dv,
+                                                           float* __restrict__ lse2) {
   constexpr int CPH = D / 8;  // 16-byte chunks per head
   const int lane = threadIdx.x & 63;
   const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -275,7 +285,11 @@ __global__ __launch_bounds__(256) void attn_bwd_pre_kernel(AttnShape sh, const b
     }
 #pragma unroll
     for (int off = CPH / 2; off >= 1; off >>= 1) acc += __shfl_xor(acc, off);
-    if (c < chunks && (c % CPH) == 0) Dv[((int64_t)b * sh.nq + c / CPH) * sh.seq + s] = acc;
+    if (c < chunks && (c % CPH) == 0) {
+      const int64_t i = ((int64_t)b * sh.nq + c / CPH) * sh.seq + s;
+      Dv[i] = acc;
+      lse2[i] = lse[i] * LOG2E;
+    }
   }
 }
 
@@ -317,17 +331,42 @@ LS_DEV void unrotate_store(const f32x16 (&acc)[D / 32], float scale, const float
 // dK and dV for 128 keys of one kv head (4 waves x 32 keys), summed over the
 // query heads of the group, no atomics.  The 1-D grid runs the key tiles with
 // the most queries after them (lowest key index) first.
+//
+// A wave issues one MFMA per slot.  Each 32-query block of a 64-query tile
+// takes four phases: S = Q K^T, dP = dO V^T, dV^T += dO^T P, dK^T += Q^T dS.
+// The softmax work is spread between the MFMAs: P = exp2(S - LSE) (and its
+// bf16 operands) during the dP phase, dS = P (dP - D) during the dV phase, so
+// the vector ALU works while the matrix core does.  Every MFMA operand read
+// from LDS is issued RA slots ahead into a ring of registers (across tile
+// boundaries too), so no MFMA waits on an LDS read.  Three LDS stages: RA
+// slots before the end of tile t each wave waits for its loads of tile t+1
+// and for the other waves (whose reads of tile t-1 are then done), and the
+// loads of tile t+2 go into tile t-1's stage.
 template <int D>
 __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnShape sh, const bf16_t* __restrict__ qkv,
                                                                 const bf16_t* __restrict__ dout,
-                                                                const float* __restrict__ lse,
+                                                                const float* __restrict__ lse2,
                                                                 const float* __restrict__ Dv, bf16_t* __restrict__ dqkv,
                                                                 const float* __restrict__ rope_cs, float scale,
                                                                 float sl2) {
-  __shared__ __attribute__((aligned(1024))) bf16_t Qs[2][BWD_BQ * D];
-  __shared__ __attribute__((aligned(1024))) bf16_t dOs[2][BWD_BQ * D];
-  __shared__ __attribute__((aligned(1024))) float Ls[2][256];
-  __shared__ __attribute__((aligned(1024))) float Ds[2][256];
+  constexpr int NST = 3;                    // LDS stages
+  constexpr int NSD = D / 16, NI = D / 32;  // 16-wide d steps; 32-row d blocks
+  constexpr int P1 = NSD, P2 = NSD, P3 = 2 * NI, P4 = 2 * NI;  // slots per phase
+  constexpr int NB = P1 + P2 + P3 + P4;     // slots of a 32-query block
+  constexpr int NSLOT = 2 * NB;
+  constexpr int RING = 8, RA = RING - 1;    // operand ring; read-ahead in slots
+  static_assert(NSLOT % RING == 0, "ring positions repeat every tile");
+  static_assert(P1 >= 4 && P2 >= 4 && 16 % P2 == 0 && 16 % P3 == 0, "phase sizes");
+  constexpr int BAR = NSLOT - RA;           // slot of the barrier
+  // one stage: Q tile, dO tile, log-sum-exp (base 2) and D of its queries
+  // (every operand of a stage within the reach of an LDS instruction's offset)
+  struct Stage {
+    bf16_t q[BWD_BQ * D];
+    bf16_t o[BWD_BQ * D];
+    float l[256];
+    float d[256];
+  };
+  __shared__ __attribute__((aligned(1024))) Stage stg[NST];
 
   const int S = sh.seq, nq = sh.nq, nkv = sh.nkv, G = nq / nkv;
   const int per = nkv * sh.batch, x = (int)blockIdx.x;
@@ -338,7 +377,8 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnShape sh, con
   const bf16_t* dbase = dout + (int64_t)b * S * ldo;
   const i32x4 rq_ = rsrc(base, clamp_bytes((int64_t)S * ld * 2));
   const i32x4 rdo = rsrc(dbase, clamp_bytes((int64_t)S * ldo * 2));
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, lr = lane & 31, lh = lane >> 5;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lr = lane & 31, lh = lane >> 5;
   const int kv0 = kvt * BWD_BKV;
   const int kvrow = kv0 + 32 * wave + lr;
 
@@ -346,77 +386,120 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnShape sh, con
   const int q_begin = kv0;  // earlier queries see none of these keys
   const int nqt = (S - q_begin + BWD_BQ - 1) / BWD_BQ;
   const int ntiles = G * nqt;
-  auto issue = [&](int t, int buf) {
+  auto issue = [&](int t, int st) {
     const int h = kvh * G + t / nqt, q0 = q_begin + (t % nqt) * BWD_BQ;
-    load_tile<D, BWD_BQ>(rq_, ld, q0, S, h * D, Qs[buf], wave, lane);
-    load_tile<D, BWD_BQ>(rdo, ldo, q0, S, h * D, dOs[buf], wave, lane);
-    if (wave == 0) load_vec64(rsrc(lse + ((int64_t)b * nq + h) * S, (uint32_t)S * 4), q0, S, Ls[buf], lane);
-    if (wave == 1) load_vec64(rsrc(Dv + ((int64_t)b * nq + h) * S, (uint32_t)S * 4), q0, S, Ds[buf], lane);
+    load_tile<D, BWD_BQ>(rq_, ld, q0, S, h * D, stg[st].q, wave, lane);
+    load_tile<D, BWD_BQ>(rdo, ldo, q0, S, h * D, stg[st].o, wave, lane);
+    if (wave == 0) load_vec64(rsrc(lse2 + ((int64_t)b * nq + h) * S, (uint32_t)S * 4), q0, S, stg[st].l, lane);
+    if (wave == 1) load_vec64(rsrc(Dv + ((int64_t)b * nq + h) * S, (uint32_t)S * 4), q0, S, stg[st].d, lane);
   };
-  if (ntiles > 0) issue(0, 0);
+  issue(0, 0);
+  if (ntiles > 1) issue(1, 1);
 
-  u32x4 kf[D / 16], vf[D / 16];
+  u32x4 kf[NSD], vf[NSD];
 #pragma unroll
-  for (int s = 0; s < D / 16; ++s) {
+  for (int s = 0; s < NSD; ++s) {
     const bool ok = kvrow < S;
     kf[s] = ok ? load16(base + (int64_t)kvrow * ld + (nq + kvh) * D + 16 * s + 8 * lh) : u32x4{0u, 0u, 0u, 0u};
     vf[s] = ok ? load16(base + (int64_t)kvrow * ld + (nq + nkv + kvh) * D + 16 * s + 8 * lh) : u32x4{0u, 0u, 0u, 0u};
   }
 
-  f32x16 dk[D / 32], dv[D / 32];
+  f32x16 dk[NI], dv[NI];
 #pragma unroll
-  for (int i = 0; i < D / 32; ++i)
+  for (int i = 0; i < NI; ++i)
 #pragma unroll
     for (int r = 0; r < 16; ++r) dk[i][r] = dv[i][r] = 0.f;
 
-  sync_lds();
-  for (int t = 0; t < ntiles; ++t) {
-    const int cur = t & 1;
-    const int q0 = q_begin + (t % nqt) * BWD_BQ;
-    if (t + 1 < ntiles) issue(t + 1, cur ^ 1);
-    if (kv0 + 32 * wave <= q0 + BWD_BQ - 1) {  // else every query of the tile precedes this wave's keys
-      f32x16 sacc[2], pacc[2];
-#pragma unroll
-      for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) sacc[qb][r] = pacc[qb][r] = 0.f;
-#pragma unroll
-      for (int s = 0; s < D / 16; ++s)
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-          sacc[qb] = mfma32(row_frag<D>(Qs[cur], 32 * qb + lr, s, lh), kf[s], sacc[qb]);
-          pacc[qb] = mfma32(row_frag<D>(dOs[cur], 32 * qb + lr, s, lh), vf[s], pacc[qb]);
-        }
-      // lane holds key kvrow, queries q0 + 32qb + 8(r/4) + 4lh + r%4
-      const bool edge = q0 < kv0 + BWD_BKV || q0 + BWD_BQ > S;
-#pragma unroll
-      for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-        for (int rq = 0; rq < 4; ++rq) {
-          const int ql = 32 * qb + 8 * rq + 4 * lh;
-          const f32x4 L = *(const f32x4*)&Ls[cur][ql];
-          const f32x4 Dd = *(const f32x4*)&Ds[cur][ql];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int r = 4 * rq + e, q = q0 + ql + e;
-            float p = ex2(fmaf(sacc[qb][r], sl2, -L[e] * LOG2E));
-            if (edge && !(kvrow <= q && q < S)) p = 0.f;
-            pacc[qb][r] = p * (pacc[qb][r] - Dd[e]);
-            sacc[qb][r] = p;
-          }
-        }
-#pragma unroll
-      for (int s = 0; s < BWD_BQ / 16; ++s) {
-        const u32x4 pf = pack_frag(sacc[s >> 1], 8 * (s & 1));
-        const u32x4 sf = pack_frag(pacc[s >> 1], 8 * (s & 1));
-#pragma unroll
-        for (int i = 0; i < D / 32; ++i) {
-          dv[i] = mfma32(colt_frag<D>(dOs[cur], 32 * i, s, lane), pf, dv[i]);
-          dk[i] = mfma32(colt_frag<D>(Qs[cur], 32 * i, s, lane), sf, dk[i]);
-        }
-      }
+  // MFMA A operand of slot j of the tile in stage st.
+  auto operand = [&](auto j_c, int st) -> u32x4 {
+    constexpr int j = decltype(j_c)::value;
+    constexpr int qb = j / NB, k = j % NB;
+    if constexpr (k < P1) return row_frag<D>(stg[st].q, 32 * qb + lr, k, lh);
+    else if constexpr (k < P1 + P2) return row_frag<D>(stg[st].o, 32 * qb + lr, k - P1, lh);
+    else if constexpr (k < P1 + P2 + P3) {
+      constexpr int c = k - P1 - P2;
+      return colt_frag<D>(stg[st].o, 32 * (c % NI), 2 * qb + c / NI, lane);
+    } else {
+      constexpr int c = k - P1 - P2 - P3;
+      return colt_frag<D>(stg[st].q, 32 * (c % NI), 2 * qb + c / NI, lane);
     }
-    sync_lds();
+  };
+
+  u32x4 ring[RING];
+  f32x16 sacc, pacc;
+  f32x4 Lq[2], Dq[2];  // base-2 log-sum-exp and D of the block's queries 8rq + 4lh + {0..3}, rq even / odd
+  u32x4 pf[2], sf[2];
+
+  // One tile in stage ST (the next tile's stage is ST+1, the one after ST+2,
+  // modulo 3): the stage is a constant, so every LDS address is a per-lane
+  // offset plus an instruction offset.
+  auto tile = [&](int t, int st, int st1, int st2) {
+    const int q0 = q_begin + (t % nqt) * BWD_BQ;
+    // causal mask: element r of block qb is query q0 + 4lh + c with
+    // c = 32qb + 8(r/4) + r%4, kept when c >= lo, i.e. q >= kvrow.  Queries
+    // past the end of the sequence need no mask: their Q, dO, LSE and D read
+    // as zero, so they add nothing to dK or dV.
+    const int lo = kvrow - q0 - 4 * lh;
+    static_for<NSLOT>([&](auto j_c) {
+      constexpr int j = decltype(j_c)::value;
+      constexpr int qb = j / NB, k = j % NB;
+      __builtin_amdgcn_sched_barrier(0);
+      if constexpr (j == BAR) {
+        LS_WAIT_VMCNT(0);
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        if (t + 2 < ntiles) issue(t + 2, st2);
+      }
+      const u32x4 a = ring[j % RING];
+      if constexpr (k < P1) {  // S = Q K^T; read the block's log-sum-exp
+        sacc = mfma32(a, kf[k], k == 0 ? f32x16{} : sacc);
+        if constexpr (k == P1 - 1) Lq[0] = *(const f32x4*)&stg[st].l[32 * qb + 4 * lh];
+      } else if constexpr (k < P1 + P2) {  // dP = dO V^T, meanwhile P = exp2(S sl2 - LSE2)
+        constexpr int c = k - P1, PER = 16 / P2;
+        pacc = mfma32(a, vf[c], c == 0 ? f32x16{} : pacc);
+        static_for<PER>([&](auto u_c) {
+          constexpr int r = c * PER + decltype(u_c)::value, rq = r >> 2, e = r & 3;
+          // the next group's log-sum-exp, one group ahead
+          if constexpr (e == 0 && rq < 3) Lq[(rq + 1) & 1] = *(const f32x4*)&stg[st].l[32 * qb + 8 * (rq + 1) + 4 * lh];
+          if constexpr (r == 12) Dq[0] = *(const f32x4*)&stg[st].d[32 * qb + 4 * lh];
+          float p = ex2(fmaf(sacc[r], sl2, -Lq[rq & 1][e]));
+          if (32 * qb + 8 * rq + e < lo) p = 0.f;
+          sacc[r] = p;
+          if constexpr ((r & 7) == 7) pf[r >> 3] = pack_frag(sacc, r - 7);
+        });
+      } else if constexpr (k < P1 + P2 + P3) {  // dV^T += dO^T P, meanwhile dS = P (dP - D)
+        constexpr int c = k - P1 - P2, PER = 16 / P3;
+        dv[c % NI] = mfma32(a, pf[c / NI], dv[c % NI]);
+        static_for<PER>([&](auto u_c) {
+          constexpr int r = c * PER + decltype(u_c)::value, rq = r >> 2, e = r & 3;
+          if constexpr (e == 0 && rq < 3) Dq[(rq + 1) & 1] = *(const f32x4*)&stg[st].d[32 * qb + 8 * (rq + 1) + 4 * lh];
+          pacc[r] = sacc[r] * (pacc[r] - Dq[rq & 1][e]);
+          if constexpr ((r & 7) == 7) sf[r >> 3] = pack_frag(pacc, r - 7);
+        });
+      } else {  // dK^T += Q^T dS
+        constexpr int c = k - P1 - P2 - P3;
+        dk[c % NI] = mfma32(a, sf[c / NI], dk[c % NI]);
+      }
+      // operand of slot j + RA (of this tile or, past its end, of the next)
+      if constexpr (j + RA < NSLOT) ring[(j + RA) % RING] = operand(std::integral_constant<int, j + RA>{}, st);
+      else ring[(j + RA) % RING] = operand(std::integral_constant<int, j + RA - NSLOT>{}, st1);
+      __builtin_amdgcn_sched_barrier(0);
+    });
+  };
+
+  LS_WAIT_VMCNT(0);
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+  static_for<RA>([&](auto j_c) { ring[decltype(j_c)::value] = operand(j_c, 0); });
+  int st = 0, st1 = 1, st2 = 2;
+  for (int t = 0; t < ntiles; ++t) {
+    tile(t, st, st1, st2);
+    const int tmp = st;
+    st = st1;
+    st1 = st2;
+    st2 = tmp;
   }
 
   // dK = scale * dS^T Q (un-rotated), dV = P^T dO.  Lane holds key kvrow.
@@ -429,13 +512,27 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnShape sh, con
 // tiles up to the diagonal, recomputes S^T and dP^T with keys as MFMA rows (a
 // lane owns one query, as in the forward), forms dS^T in registers and
 // accumulates dQ^T += K^T dS^T.
+//
+// Per 64-key tile a wave issues one MFMA per slot: S^T and dP^T of key block 0,
+// then of key block 1, then dQ^T for block 0 and for block 1.  The softmax work
+// of block 0 (P = exp2(S - LSE), dS = P (dP - D), bf16 operands) runs between
+// the MFMAs of block 1's S^T and dP^T, that of block 1 between the MFMAs of
+// block 0's dQ^T.  MFMA operands from LDS are read RA slots ahead into a ring
+// of registers within the tile; two workgroups per compute unit keep the
+// matrix cores busy across tile boundaries and while one wave waits.
 template <int D>
 __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(AttnShape sh, const bf16_t* __restrict__ qkv,
                                                               const bf16_t* __restrict__ dout,
-                                                              const float* __restrict__ lse,
+                                                              const float* __restrict__ lse2,
                                                               const float* __restrict__ Dv, bf16_t* __restrict__ dqkv,
                                                               const float* __restrict__ rope_cs, float scale,
                                                               float sl2) {
+  constexpr int NSD = D / 16, NI = D / 32;
+  constexpr int PS = 2 * NSD;                // slots of one block's S^T and dP^T (interleaved)
+  constexpr int PQ = 2 * NI;                 // slots of one block's dQ^T
+  constexpr int NSLOT = 2 * PS + 2 * PQ;
+  constexpr int RING = 2, RA = RING - 1;
+  static_assert(NSLOT % RING == 0 && 16 % PS == 0 && 16 % PQ == 0, "slot counts");
   __shared__ __attribute__((aligned(1024))) bf16_t Ks[2][BKV * D];
   __shared__ __attribute__((aligned(1024))) bf16_t Vs[2][BKV * D];
 
@@ -446,10 +543,10 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(AttnShape sh, const
   const int64_t ldo = (int64_t)nq * D;
   const bf16_t* base = qkv + (int64_t)b * S * ld;
   const i32x4 rs = rsrc(base, clamp_bytes((int64_t)S * ld * 2));
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, lr = lane & 31, lh = lane >> 5;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lr = lane & 31, lh = lane >> 5;
   const int q0 = qtile.qt * BQ;
   const int qrow = q0 + 32 * wave + lr;
-  const int wave_qmin = q0 + 32 * wave, wave_qmax = wave_qmin + 31;
   const bool qok = qrow < S;
   const int kcol = (nq + kvh) * D, vcol = (nq + nkv + kvh) * D;
 
@@ -458,20 +555,47 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(AttnShape sh, const
   load_tile<D, BKV>(rs, ld, 0, S, kcol, Ks[0], wave, lane);
   load_tile<D, BKV>(rs, ld, 0, S, vcol, Vs[0], wave, lane);
 
-  u32x4 qf[D / 16], df[D / 16];
+  u32x4 qf[NSD], df[NSD];
 #pragma unroll
-  for (int s = 0; s < D / 16; ++s) {
+  for (int s = 0; s < NSD; ++s) {
     qf[s] = qok ? load16(base + (int64_t)qrow * ld + h * D + 16 * s + 8 * lh) : u32x4{0u, 0u, 0u, 0u};
     df[s] = qok ? load16(dout + ((int64_t)b * S + qrow) * ldo + h * D + 16 * s + 8 * lh) : u32x4{0u, 0u, 0u, 0u};
   }
-  const float lse2 = qok ? lse[((int64_t)b * nq + h) * S + qrow] * LOG2E : 0.f;
+  const float L2 = qok ? lse2[((int64_t)b * nq + h) * S + qrow] : 0.f;
   const float Dq = qok ? Dv[((int64_t)b * nq + h) * S + qrow] : 0.f;
 
-  f32x16 dq[D / 32];
+  f32x16 dq[NI];
 #pragma unroll
-  for (int i = 0; i < D / 32; ++i)
+  for (int i = 0; i < NI; ++i)
 #pragma unroll
     for (int r = 0; r < 16; ++r) dq[i][r] = 0.f;
+
+  // MFMA A operand of slot j of the tile in stage st.
+  auto operand = [&](auto j_c, int st) -> u32x4 {
+    constexpr int j = decltype(j_c)::value;
+    if constexpr (j < 2 * PS) {
+      constexpr int bb = j / PS, k = j % PS;
+      return row_frag<D>((k & 1) ? Vs[st] : Ks[st], 32 * bb + lr, k >> 1, lh);
+    } else {
+      constexpr int bb = (j - 2 * PS) / PQ, c = (j - 2 * PS) % PQ;
+      return colt_frag<D>(Ks[st], 32 * (c % NI), 2 * bb + c / NI, lane);
+    }
+  };
+
+  u32x4 ring[RING];
+  f32x16 sacc[2], pacc[2];
+  u32x4 sf[2][2];
+  // causal mask: element r of key block bb is key kv0 + 4lh + c with
+  // c = 32bb + 8(r/4) + r%4, kept when c <= hi, i.e. key <= qrow.  Keys past the
+  // end of the sequence need no mask beyond that: their K and V read as zero.
+  auto soft = [&](auto bb_c, auto r_c, int hi) {
+    constexpr int bb = decltype(bb_c)::value, r = decltype(r_c)::value;
+    constexpr int c = 32 * bb + 8 * (r >> 2) + (r & 3);
+    float p = ex2(fmaf(sacc[bb][r], sl2, -L2));
+    if (c > hi) p = 0.f;
+    pacc[bb][r] = p * (pacc[bb][r] - Dq);
+    if constexpr ((r & 7) == 7) sf[bb][r >> 3] = pack_frag(pacc[bb], r - 7);
+  };
 
   sync_lds();
   for (int kt = 0; kt < nkt; ++kt) {
@@ -480,37 +604,35 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(AttnShape sh, const
       load_tile<D, BKV>(rs, ld, kv0 + BKV, S, kcol, Ks[cur ^ 1], wave, lane);
       load_tile<D, BKV>(rs, ld, kv0 + BKV, S, vcol, Vs[cur ^ 1], wave, lane);
     }
-    if (kv0 <= wave_qmax) {
-      f32x16 sacc[BKV / 32], pacc[BKV / 32];
-#pragma unroll
-      for (int bb = 0; bb < BKV / 32; ++bb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) sacc[bb][r] = pacc[bb][r] = 0.f;
-#pragma unroll
-      for (int s = 0; s < D / 16; ++s)
-#pragma unroll
-        for (int bb = 0; bb < BKV / 32; ++bb) {
-          sacc[bb] = mfma32(row_frag<D>(Ks[cur], 32 * bb + lr, s, lh), qf[s], sacc[bb]);
-          pacc[bb] = mfma32(row_frag<D>(Vs[cur], 32 * bb + lr, s, lh), df[s], pacc[bb]);
+    const int hi = qrow - kv0 - 4 * lh;
+    static_for<RA>([&](auto j_c) { ring[decltype(j_c)::value] = operand(j_c, cur); });
+    static_for<NSLOT>([&](auto j_c) {
+      constexpr int j = decltype(j_c)::value;
+      __builtin_amdgcn_sched_barrier(0);
+      const u32x4 a = ring[j % RING];
+      if constexpr (j < 2 * PS) {
+        constexpr int bb = j / PS, k = j % PS, s = k >> 1;
+        if constexpr (k & 1) pacc[bb] = mfma32(a, df[s], s == 0 ? f32x16{} : pacc[bb]);
+        else sacc[bb] = mfma32(a, qf[s], s == 0 ? f32x16{} : sacc[bb]);
+        if constexpr (bb == 1) {  // softmax of block 0
+          constexpr int PER = 16 / PS;
+          static_for<PER>([&](auto u) {
+            soft(std::integral_constant<int, 0>{}, std::integral_constant<int, k * PER + decltype(u)::value>{}, hi);
+          });
         }
-      // lane holds query qrow, keys kv0 + 32bb + 8(r/4) + 4lh + r%4
-      const bool diag = kv0 + BKV - 1 > wave_qmin;
-#pragma unroll
-      for (int bb = 0; bb < BKV / 32; ++bb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int kv = kv0 + 32 * bb + 8 * (r >> 2) + 4 * lh + (r & 3);
-          float p = ex2(fmaf(sacc[bb][r], sl2, -lse2));
-          if (diag && kv > qrow) p = 0.f;
-          pacc[bb][r] = p * (pacc[bb][r] - Dq);
+      } else {
+        constexpr int bb = (j - 2 * PS) / PQ, c = (j - 2 * PS) % PQ;
+        dq[c % NI] = mfma32(a, sf[bb][c / NI], dq[c % NI]);
+        if constexpr (bb == 0) {  // softmax of block 1
+          constexpr int PER = 16 / PQ;
+          static_for<PER>([&](auto u) {
+            soft(std::integral_constant<int, 1>{}, std::integral_constant<int, c * PER + decltype(u)::value>{}, hi);
+          });
         }
-#pragma unroll
-      for (int s = 0; s < BKV / 16; ++s) {
-        const u32x4 sf = pack_frag(pacc[s >> 1], 8 * (s & 1));
-#pragma unroll
-        for (int i = 0; i < D / 32; ++i) dq[i] = mfma32(colt_frag<D>(Ks[cur], 32 * i, s, lane), sf, dq[i]);
       }
-    }
+      if constexpr (j + RA < NSLOT) ring[(j + RA) % RING] = operand(std::integral_constant<int, j + RA>{}, cur);
+      __builtin_amdgcn_sched_barrier(0);
+    });
     sync_lds();
   }
   if (!qok) return;
@@ -530,18 +652,21 @@ hipError_t attn_bwd_t(const AttnShape& sh, const bf16_t* qkv, const bf16_t* o, c
                       bf16_t* dqkv, const float* rope_cs, void* ws, hipStream_t s) {
   const int64_t T = (int64_t)sh.batch * sh.seq;
   float* Dv = (float*)ws;
-  hipLaunchKernelGGL((attn_bwd_pre_kernel<D>), dim3((unsigned)((T + 3) / 4)), dim3(256), 0, s, sh, o, dout, Dv);
+  float* lse2 = Dv + T * sh.nq;
+  hipLaunchKernelGGL((attn_bwd_pre_kernel<D>), dim3((unsigned)((T + 3) / 4)), dim3(256), 0, s, sh, o, dout, lse, Dv,
+                     lse2);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const float scale = 1.0f / sqrtf((float)D);
   const unsigned gkv = (unsigned)((sh.seq + BWD_BKV - 1) / BWD_BKV) * sh.nkv * sh.batch;
-  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D>), dim3(gkv), dim3(256), 0, s, sh, qkv, dout, lse, (const float*)Dv,
+  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D>), dim3(gkv), dim3(256), 0, s, sh, qkv, dout, (const float*)lse2,
+                     (const float*)Dv,
                      dqkv, rope_cs, scale, scale * LOG2E);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   const unsigned gq = (unsigned)((sh.seq + BQ - 1) / BQ) * sh.nq * sh.batch;
-  hipLaunchKernelGGL((attn_bwd_dq_kernel<D>), dim3(gq), dim3(256), 0, s, sh, qkv, dout, lse, (const float*)Dv, dqkv,
-                     rope_cs, scale, scale * LOG2E);
+  hipLaunchKernelGGL((attn_bwd_dq_kernel<D>), dim3(gq), dim3(256), 0, s, sh, qkv, dout, (const float*)lse2,
+                     (const float*)Dv, dqkv, rope_cs, scale, scale * LOG2E);
   return hipGetLastError();
 }
 
@@ -555,7 +680,7 @@ hipError_t attn_fwd(const AttnShape& sh, const bf16_t* qkv, bf16_t* o, float* ls
 
 size_t attn_bwd_workspace(const AttnShape& sh) {
   const int64_t T = (int64_t)sh.batch * sh.seq;
-  return (size_t)(T * sh.nq) * sizeof(float);
+  return 2 * (size_t)(T * sh.nq) * sizeof(float);  // D, then the base-2 log-sum-exp
 }
 
 hipError_t attn_bwd(const AttnShape& sh, const bf16_t* qkv, const bf16_t* o, const float* lse, const bf16_t* dout,

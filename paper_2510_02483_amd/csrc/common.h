@@ -4,6 +4,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+#include <utility>
+
 typedef uint16_t bf16_t;
 typedef __bf16 bf16x8_v __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -13,6 +16,18 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 #define LS_DEV __device__ __forceinline__
 
+// f(integral_constant<int, 0>), ..., f(integral_constant<int, N-1>): a loop
+// unrolled at compile time, so that indices into register arrays and the
+// schedule of every slot are constants whatever the size of the body.
+template <class F, int... I>
+LS_DEV void static_for_(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, class F>
+LS_DEV void static_for(F&& f) {
+  static_for_(f, std::make_integer_sequence<int, N>{});
+}
+
 LS_DEV float bf2f(uint32_t b16) { return __uint_as_float(b16 << 16); }
 LS_DEV float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
 LS_DEV float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
@@ -20,7 +35,13 @@ LS_DEV float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 // float -> bf16 bits, round to nearest even (the compiler's conversion, which
 // gfx950 executes as a hardware convert).
 LS_DEV uint32_t f2bf(float f) { return (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)f); }
-LS_DEV uint32_t pack_bf2(float lo, float hi) { return f2bf(lo) | (f2bf(hi) << 16); }
+typedef __bf16 bf16x2_v __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+// Two floats -> two bf16 (RNE) in one word, lo in the low half: one packed
+// hardware convert.
+LS_DEV uint32_t pack_bf2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){lo, hi}, bf16x2_v));
+}
 
 // D(32x32, fp32) += A(32x16) * B(16x32), bf16 operands.  Lane l supplies
 // A[l%32][8*(l/32) .. +7] in `a` and B[8*(l/32) .. +7][l%32] in `b`; it holds

@@ -61,18 +61,6 @@ constexpr uint32_t OOB = LS_OOB;
 #endif
 
 
-// f(integral_constant<int, 0>), ..., f(integral_constant<int, N-1>): a loop
-// unrolled at compile time, so that indices into register arrays and the
-// schedule of every slot are constants whatever the size of the body.
-template <class F, int... I>
-LS_DEV void static_for_(F&& f, std::integer_sequence<int, I...>) {
-  (f(std::integral_constant<int, I>{}), ...);
-}
-template <int N, class F>
-LS_DEV void static_for(F&& f) {
-  static_for_(f, std::make_integer_sequence<int, N>{});
-}
-
 // Launch order: workgroups are handed to the 8 XCDs round-robin, so first
 // renumber them so that each XCD receives a contiguous range of logical tiles,
 // then walk the tiles in groups of GROUP_M tile rows so that the tiles an XCD

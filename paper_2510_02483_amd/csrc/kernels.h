@@ -76,7 +76,7 @@ struct AttnShape {
   int batch, seq, nq, nkv, d;
 };
 hipError_t attn_fwd(const AttnShape& sh, const bf16_t* qkv, bf16_t* o, float* lse, hipStream_t s);
-// Workspace for attn_bwd: D [batch*nq*seq] fp32.
+// Workspace for attn_bwd: D and the base-2 log-sum-exp, [batch*nq*seq] fp32 each.
 size_t attn_bwd_workspace(const AttnShape& sh);
 // rope_cs may be null (no inverse rotation of dq and dk).
 hipError_t attn_bwd(const AttnShape& sh, const bf16_t* qkv, const bf16_t* o, const float* lse,
