@@ -139,3 +139,67 @@ def test_block_3b_full_size_sampled():
     ya = f64(y_all).reshape(4, c.seq, c.hidden)[perm]
     yb = f64(blk2.y).reshape(4, c.seq, c.hidden)
     assert np.array_equal(ya, yb)
+
+
+def _prefix_parity(c, t0, sample_seq=0):
+    """The block at its full size and launch configuration, checked against
+    the oracle on the first t0 tokens of one sequence.  The upstream gradient
+    is zero past t0 and on every other sequence, so (causality) the outputs
+    of the first t0 tokens, dx of those tokens and every weight gradient are
+    those of the t0-token sequence alone, and dx is exactly zero past t0."""
+    host = inputs.make_inputs(c)
+    full = host["dy"].clone()
+    host["dy"].zero_()
+    host["dy"][sample_seq, :t0] = full[sample_seq, :t0]
+    blk = L.Block(c, host)
+    blk.step()
+    torch.cuda.synchronize()
+    one = c.with_(batch=1, seq=t0)
+    f = inputs.to_f64({k: (v[sample_seq:sample_seq + 1, :t0] if k in ("x", "dy") else v) for k, v in host.items()})
+    say(f"  oracle on sequence {sample_seq}, tokens 0..{t0 - 1} ...")
+    fwd, gr = oracle_block(one, f)
+    shp = (c.batch, c.seq, c.hidden)
+    y = f64(blk.y).reshape(shp)[sample_seq:sample_seq + 1, :t0]
+    dx_all = f64(blk.dx).reshape(shp)
+    dx = dx_all[sample_seq:sample_seq + 1, :t0]
+    errs = {"y": max_rel(y, fwd["y"]), "dx": fro_rel(dx, gr["dx"])}
+    for n in GRAD_NAMES:
+        errs[n] = fro_rel(f64(blk.grads[n]), gr[n])
+    say("  errors:", {k: f"{v:.2e}" for k, v in errs.items()})
+    assert errs["y"] < OUT_TOL, errs
+    for k, v in errs.items():
+        if k != "y":
+            assert v < GRAD_TOL, (k, errs)
+    # no upstream gradient past t0 (or on the other sequences): no input gradient there
+    rest = dx_all.copy()
+    rest[sample_seq, :t0] = 0
+    assert np.count_nonzero(rest) == 0
+    return blk, host
+
+
+def test_block_3b_8k_full_size_prefix():
+    """The 3B block at long context (batch 1 x seq 8192), full launch
+    configuration; oracle on the first 1024 tokens (the fp64 oracle of the
+    whole 8k sequence takes minutes)."""
+    need_gpu()
+    c = configs.B3_8K
+    say(f"3b_8k full size {c}")
+    _prefix_parity(c, 1024)
+
+
+def test_block_30b_full_size_prefix():
+    """The Llama-30B-shaped block (batch 2 x seq 2048, 52 MHA heads, SwiGLU
+    17920) at full size; oracle on the first 512 tokens of sequence 1, and the
+    batch swapped gives the outputs swapped exactly."""
+    need_gpu()
+    c = configs.B30
+    say(f"30b full size {c}")
+    blk, host = _prefix_parity(c, 512, sample_seq=1)
+    y_all = f64(blk.y).reshape(c.batch, c.seq, c.hidden)
+    del blk
+    host2 = dict(host)
+    host2["x"] = host["x"][[1, 0]].contiguous()
+    blk2 = L.Block(c, host2)
+    blk2.step()
+    torch.cuda.synchronize()
+    assert np.array_equal(y_all[[1, 0]], f64(blk2.y).reshape(c.batch, c.seq, c.hidden))

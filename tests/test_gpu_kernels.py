@@ -134,3 +134,41 @@ def test_attention_core(name, B, S, nq, nkv, d, std):
         return
     assert fro_rel(g[:, :Dq], dq.reshape(T, Dq)) < GRAD_TOL
     assert fro_rel(g[:, Dq:Dq + Dkv], dk.reshape(T, Dkv)) < GRAD_TOL
+
+
+def test_attention_core_8k_sampled_group():
+    """Attention at the long-context shape (1 x 8192, 24 query heads / 8 kv
+    heads x 128) in its full launch configuration; the oracle computes one kv
+    group (kv head 5 and its query heads 15..17) over all 8192 positions."""
+    need_gpu()
+    B, S, nq, nkv, d = 1, 8192, 24, 8, 128
+    G = nq // nkv
+    kvh = 5
+    say("attention core 8k, kv group 5")
+    c = configs.TINY.with_(batch=B, seq=S, n_q_heads=nq, n_kv_heads=nkv, head_dim=d, hidden=nq * d)
+    T, Dq, Dkv = B * S, nq * d, nkv * d
+    q = bf16_randn((T, Dq), 21)
+    k = bf16_randn((T, Dkv), 22)
+    v = bf16_randn((T, Dkv), 23)
+    qkv = torch.cat([q, k, v], dim=1).contiguous()
+    o = torch.empty((T, Dq), dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty((B, nq, S), dtype=torch.float32, device="cuda")
+    L.ls_attn_core_fwd(c, qkv, o, lse)
+    do = bf16_randn((T, Dq), 24)
+    dqkv = torch.empty_like(qkv)
+    ws = torch.empty(L.ls_attn_core_bwd_workspace(c), dtype=torch.uint8, device="cuda")
+    L.ls_attn_core_bwd(c, qkv, o, lse, do, dqkv, ws)
+    torch.cuda.synchronize()
+    hs = slice(kvh * G, (kvh + 1) * G)
+    q4 = f64(q).reshape(B, S, nq, d)[:, :, hs]
+    k4 = f64(k).reshape(B, S, nkv, d)[:, :, kvh:kvh + 1]
+    v4 = f64(v).reshape(B, S, nkv, d)[:, :, kvh:kvh + 1]
+    oref, lref = ob.attention_forward(q4, k4, v4)
+    og = f64(o).reshape(B, S, nq, d)[:, :, hs]
+    assert max_rel(og, oref) < OUT_TOL
+    assert np.max(np.abs(f64(lse)[:, hs] - lref)) < 1e-3 * max(1.0, np.max(np.abs(lref)))
+    dq, dk, dv = ob.attention_backward(f64(do).reshape(B, S, nq, d)[:, :, hs], q4, k4, v4)
+    g = f64(dqkv)
+    assert fro_rel(g[:, :Dq].reshape(B, S, nq, d)[:, :, hs], dq) < GRAD_TOL
+    assert fro_rel(g[:, Dq:Dq + Dkv].reshape(B, S, nkv, d)[:, :, kvh:kvh + 1], dk) < GRAD_TOL
+    assert fro_rel(g[:, Dq + Dkv:].reshape(B, S, nkv, d)[:, :, kvh:kvh + 1], dv) < GRAD_TOL
