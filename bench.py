@@ -24,7 +24,7 @@ METRIC = "decoder-block fwd+bwd TFLOP/s and MFU (bf16), 3B shape seq 2048, 1 MI3
 PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 matrix peak (256 CUs x 4096 FLOP/clk x 2.4 GHz)
 PEAK_HBM_GBS = 8000.0
 DOMINANT = "gate/up projection"  # the largest single kernel launch of the step
-DOMINANT_KERNEL = "gemm_kernel<true, true, 3>"  # its HIP kernel (gate/up product + SwiGLU epilogue)
+DOMINANT_KERNEL = "gemm_kernel<true, true, 3, 256, 256>"  # its HIP kernel (gate/up product + SwiGLU epilogue)
 COPY_BYTES = 1 << 30  # size of the plain device copy used to calibrate the HBM byte counters
 
 
@@ -90,6 +90,53 @@ def cpu_baseline(c, sequences: int):
                       f"(BLAS matmuls), {dt:.1f} s wall"}
 
 
+def kernel_only(args):
+    """Time one kernel family through the C ABI on seeded inputs (for
+    per-kernel counters): a plain bf16 product C = A B^T of --shape M,N,K, or
+    causal attention forward + backward at the configuration's shape."""
+    import torch
+
+    from paper_2510_02483_amd import configs, flops, lib
+
+    g = torch.Generator(device="cpu").manual_seed(1234)
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def timed(fn, n):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        start.record()
+        for _ in range(n):
+            fn()
+        stop.record()
+        torch.cuda.synchronize()
+        return start.elapsed_time(stop) / n
+
+    if args.kernel == "gemm_nt":
+        M, N, K = (int(v) for v in args.shape.split(","))
+        A = torch.randn(M, K, generator=g).to(torch.bfloat16).cuda()
+        B = torch.randn(N, K, generator=g).to(torch.bfloat16).cuda()
+        C = torch.empty(M, N, dtype=torch.bfloat16, device="cuda")
+        ms = timed(lambda: lib.ls_gemm_nt(A, B, C), args.steps)
+        out = {"kernel": "gemm_nt", "shape": [M, N, K], "ms": round(ms, 4),
+               "tflops": round(2.0 * M * N * K / (ms * 1e-3) / 1e12, 2)}
+    else:
+        c = configs.PRESETS[args.config]
+        T, Dq, Dkv = c.tokens, c.dq, c.dkv
+        qkv = torch.randn(T, Dq + 2 * Dkv, generator=g).to(torch.bfloat16).cuda()
+        do = torch.randn(T, Dq, generator=g).to(torch.bfloat16).cuda()
+        o = torch.empty(T, Dq, dtype=torch.bfloat16, device="cuda")
+        lse = torch.empty(c.batch, c.n_q_heads, c.seq, dtype=torch.float32, device="cuda")
+        dqkv = torch.empty_like(qkv)
+        ws = torch.empty(lib.ls_attn_core_bwd_workspace(c), dtype=torch.uint8, device="cuda")
+        fwd = timed(lambda: lib.ls_attn_core_fwd(c, qkv, o, lse), args.steps)
+        bwd = timed(lambda: lib.ls_attn_core_bwd(c, qkv, o, lse, do, dqkv, ws), args.steps)
+        fl = flops.attention_fwd_flops(c)
+        out = {"kernel": "attention", "config": c.name, "fwd_ms": round(fwd, 4), "bwd_ms": round(bwd, 4),
+               "fwd_tflops": round(fl / (fwd * 1e-3) / 1e12, 2), "bwd_tflops_model": round(2 * fl / (bwd * 1e-3) / 1e12, 2)}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -100,6 +147,9 @@ def main():
     ap.add_argument("--cpu-sequences", type=int, default=4, help="sequences in the oracle's timed sample")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run only a plain 1 GiB device copy (for counter calibration) and exit")
+    ap.add_argument("--kernel", choices=("gemm_nt", "attention"),
+                    help="time one kernel family instead of the block step (for per-kernel counters)")
+    ap.add_argument("--shape", default="8192,16384,3072", help="M,N,K of --kernel gemm_nt")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -109,6 +159,9 @@ def main():
 
     if args.calibrate_copy:
         calibrate_copy()
+        return
+    if args.kernel:
+        kernel_only(args)
         return
 
     import torch

@@ -27,6 +27,12 @@ def block_fwd_bwd_flops(cfg: BlockConfig, causal: bool = True) -> float:
     return 3.0 * block_fwd_flops(cfg, causal)
 
 
+def attention_fwd_flops(cfg: BlockConfig, causal: bool = True) -> float:
+    """QK^T and PV of the attention forward pass (model FLOPs)."""
+    pairs = cfg.seq * (cfg.seq + 1) / 2 if causal else float(cfg.seq) ** 2
+    return 4.0 * cfg.batch * cfg.n_q_heads * cfg.head_dim * pairs
+
+
 def attention_fwd_bwd_flops(cfg: BlockConfig, causal: bool = True) -> float:
     pairs = cfg.seq * (cfg.seq + 1) / 2 if causal else float(cfg.seq) ** 2
     return 3.0 * 4.0 * cfg.batch * cfg.n_q_heads * cfg.head_dim * pairs
