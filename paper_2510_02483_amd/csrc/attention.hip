@@ -81,15 +81,14 @@ LS_DEV int tile_swz(int r) {
 // resource r) into an LDS tile; rows at or past `rows` read as zero.  Each
 // load fills 1 KB of the tile (64/(D/8) rows); wave w fills the consecutive
 // blocks w*PER .. w*PER+PER-1 with one M0 write.
-template <int D, int ROWS>
+// With REMAT the per-lane offsets are recomputed at every call from the lane
+// index (itself recomputed here) rather than hoisted out of the tile loop,
+// where they would hold registers for the whole loop.
+template <int D, int ROWS, bool REMAT = false>
 LS_DEV void load_tile(i32x4 r, int64_t ld, int row0, int rows, int col0, bf16_t* t, int wave, int lane) {
   constexpr int CPR = D / 8, RPI = 64 / CPR, NI = ROWS / RPI, PER = NI / 4;
   static_assert(NI % 4 == 0 && (PER == 2 || PER == 4), "loads split evenly over 4 waves in groups of 2 or 4");
-  // The per-lane offsets are recomputed at every call from the lane index
-  // (itself recomputed here) rather than hoisted out of the tile loop, where
-  // they would hold registers for the whole loop.
-  (void)lane;
-  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(lane));
+  if constexpr (REMAT) asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(lane));
   DmaLoad l[PER];
 #pragma unroll
   for (int jj = 0; jj < PER; ++jj) {
@@ -388,8 +387,8 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnShape sh, con
   const int ntiles = G * nqt;
   auto issue = [&](int t, int st) {
     const int h = kvh * G + t / nqt, q0 = q_begin + (t % nqt) * BWD_BQ;
-    load_tile<D, BWD_BQ>(rq_, ld, q0, S, h * D, stg[st].q, wave, lane);
-    load_tile<D, BWD_BQ>(rdo, ldo, q0, S, h * D, stg[st].o, wave, lane);
+    load_tile<D, BWD_BQ, true>(rq_, ld, q0, S, h * D, stg[st].q, wave, lane);
+    load_tile<D, BWD_BQ, true>(rdo, ldo, q0, S, h * D, stg[st].o, wave, lane);
     if (wave == 0) load_vec64(rsrc(lse2 + ((int64_t)b * nq + h) * S, (uint32_t)S * 4), q0, S, stg[st].l, lane);
     if (wave == 1) load_vec64(rsrc(Dv + ((int64_t)b * nq + h) * S, (uint32_t)S * 4), q0, S, stg[st].d, lane);
   };
@@ -552,8 +551,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(AttnShape sh, const
 
   const int kv_end = min(S, q0 + BQ);
   const int nkt = (kv_end + BKV - 1) / BKV;
-  load_tile<D, BKV>(rs, ld, 0, S, kcol, Ks[0], wave, lane);
-  load_tile<D, BKV>(rs, ld, 0, S, vcol, Vs[0], wave, lane);
+  load_tile<D, BKV, true>(rs, ld, 0, S, kcol, Ks[0], wave, lane);
+  load_tile<D, BKV, true>(rs, ld, 0, S, vcol, Vs[0], wave, lane);
 
   u32x4 qf[NSD], df[NSD];
 #pragma unroll
@@ -601,8 +600,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(AttnShape sh, const
   for (int kt = 0; kt < nkt; ++kt) {
     const int cur = kt & 1, kv0 = kt * BKV;
     if (kt + 1 < nkt) {
-      load_tile<D, BKV>(rs, ld, kv0 + BKV, S, kcol, Ks[cur ^ 1], wave, lane);
-      load_tile<D, BKV>(rs, ld, kv0 + BKV, S, vcol, Vs[cur ^ 1], wave, lane);
+      load_tile<D, BKV, true>(rs, ld, kv0 + BKV, S, kcol, Ks[cur ^ 1], wave, lane);
+      load_tile<D, BKV, true>(rs, ld, kv0 + BKV, S, vcol, Vs[cur ^ 1], wave, lane);
     }
     const int hi = qrow - kv0 - 4 * lh;
     static_for<RA>([&](auto j_c) { ring[decltype(j_c)::value] = operand(j_c, cur); });

@@ -197,6 +197,28 @@ LS_DEV u32x4 frag_ks(const bf16_t* lds, int c32, int s, int lane) {
   return out;
 }
 
+// 16 bytes (8 consecutive bf16) of row lr per lane from the MFMA layout: the
+// lane holds columns 8q + 4lh .. +3 of one row for q = 2pp, 2pp+1 (packed in
+// w0 and w1); lanes lr and lr + 32 swap halves (v_permlane32_swap: lanes 32..63
+// of the first operand trade places with lanes 0..31 of the second), after
+// which the lane holds columns 16pp + 8lh .. +7.
+LS_DEV u32x4 swap_pack(u32x2 w0, u32x2 w1) {
+  const auto x = __builtin_amdgcn_permlane32_swap(w0[0], w1[0], false, false);
+  const auto y = __builtin_amdgcn_permlane32_swap(w0[1], w1[1], false, false);
+  return u32x4{x[0], y[0], x[1], y[1]};
+}
+// The same for fp32 values: v0, v1 hold columns 8q + 4lh .. +3 (q = 2pp,
+// 2pp+1); afterwards lo and hi hold columns 16pp + 8lh + 0..3 and + 4..7.
+LS_DEV void swap_f32(f32x4 v0, f32x4 v1, f32x4& lo, f32x4& hi) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const auto t = __builtin_amdgcn_permlane32_swap(__float_as_uint(v0[e]), __float_as_uint(v1[e]), false, false);
+    lo[e] = __uint_as_float(t[0]);
+    hi[e] = __uint_as_float(t[1]);
+  }
+}
+LS_DEV u32x2 pack4(float a, float b, float c, float d) { return u32x2{pack_bf2(a, b), pack_bf2(c, d)}; }
+
 template <bool AK, bool BKC, int EPI, int BM, int BN>
 __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
   constexpr int WM = BM / 2, WN = BN / 2;  // wave tile
@@ -436,41 +458,54 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
     }
   };
 
-  if constexpr (EPI == EPI_F32 || EPI == EPI_RESID) {
-    // fp32 staging per 32-row block; the residual / old gradient is read coalesced.
-    constexpr int CH = WN / 4;  // 16-byte chunks per staged row
+  if constexpr (EPI == EPI_F32) {
+    // fp32 weight gradients straight from the registers: a lane's 4 columns are
+    // 16 contiguous bytes (read-modify-write with accumulate)
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
+      const int m = mw + 32 * i + lr;
+      const int sg = m >= p.f_start[2] ? 2 : (m >= p.f_start[1] ? 1 : 0);
+      float* base = sg == 2 ? p.F[2] : (sg == 1 ? p.F[1] : p.F[0]);
+      const int fs = sg == 2 ? p.f_start[2] : (sg == 1 ? p.f_start[1] : 0);
+      float* row = base + (int64_t)(m - fs) * p.ldf;
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int n = nw + 32 * j + 8 * q + 4 * lh;
+          f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+          if (m < p.M && n < p.N) {
+            if (p.accumulate) v += *(const f32x4*)(row + n);
+            *(f32x4*)(row + n) = v;
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  } else if constexpr (EPI == EPI_RESID) {
+    // Straight from the registers: the fp32 results are moved into 16-byte
+    // row pieces (8 columns per lane), added to the residual (one 16-byte
+    // load) and rounded once.
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const int m = mw + 32 * i + lr;
 #pragma unroll
       for (int j = 0; j < TN; ++j)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
-          *(f32x4*)&stgf[sf(lr, 32 * j + 8 * q + 4 * lh)] = v;
-        }
-#pragma unroll 4
-      for (int t = 0; t < CH / 2; ++t) {
-        const int c = lane + 64 * t, r = c / CH, cc = c % CH;
-        f32x4 v = *(const f32x4*)&stgf[sf(r, cc * 4)];
-        const int m = mw + 32 * i + r, n = nw + cc * 4;
-        if (m < p.M && n < p.N) {
-          if constexpr (EPI == EPI_F32) {
-            const int sg = m >= p.f_start[2] ? 2 : (m >= p.f_start[1] ? 1 : 0);
-            float* base = sg == 2 ? p.F[2] : (sg == 1 ? p.F[1] : p.F[0]);
-            const int fs = sg == 2 ? p.f_start[2] : (sg == 1 ? p.f_start[1] : 0);
-            float* dst = base + (int64_t)(m - fs) * p.ldf + n;
-            if (p.accumulate) v += *(const f32x4*)dst;
-            *(f32x4*)dst = v;
-          } else {
-            const u32x2 rw = *(const u32x2*)(p.R + (int64_t)m * p.ldc + n);
-            v[0] += bf_lo(rw[0]);
-            v[1] += bf_hi(rw[0]);
-            v[2] += bf_lo(rw[1]);
-            v[3] += bf_hi(rw[1]);
-            *(u32x2*)(p.C + (int64_t)m * p.ldc + n) = u32x2{pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3])};
+        for (int pp = 0; pp < 2; ++pp) {
+          const int n = nw + 32 * j + 16 * pp + 8 * lh;
+          f32x4 lo, hi;
+          swap_f32(f32x4{acc[i][j][8 * pp], acc[i][j][8 * pp + 1], acc[i][j][8 * pp + 2], acc[i][j][8 * pp + 3]},
+                   f32x4{acc[i][j][8 * pp + 4], acc[i][j][8 * pp + 5], acc[i][j][8 * pp + 6], acc[i][j][8 * pp + 7]},
+                   lo, hi);
+          if (m < p.M && n < p.N) {
+            const u32x4 rw = *(const u32x4*)(p.R + (int64_t)m * p.ldc + n);
+            *(u32x4*)(p.C + (int64_t)m * p.ldc + n) =
+                u32x4{pack_bf2(lo[0] + bf_lo(rw[0]), lo[1] + bf_hi(rw[0])), pack_bf2(lo[2] + bf_lo(rw[1]), lo[3] + bf_hi(rw[1])),
+                      pack_bf2(hi[0] + bf_lo(rw[2]), hi[1] + bf_hi(rw[2])), pack_bf2(hi[2] + bf_lo(rw[3]), hi[3] + bf_hi(rw[3]))};
           }
+          __builtin_amdgcn_sched_barrier(0);
         }
-      }
     }
   } else if constexpr (EPI == EPI_GLU_FWD) {
     static_assert(WN == 128, "gate/up interleave needs 128-column wave tiles");
@@ -520,11 +555,13 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
     static_assert(WN == 128, "the gate/up staging covers 128-column wave tiles");
     // acc = dact.  Per 32-row block: the saved gate and up values are read
     // coalesced into LDS, dg = dact u silu'(g) and du = dact silu(g) replace
-    // them in place, and both go out coalesced.
+    // them in place, and both go out coalesced.  The reads run two blocks
+    // ahead (in registers the main loop no longer needs), so each block's
+    // values have arrived when it is processed.
     bf16_t* sg_ = stg;             // gate / dg rows (32 x 128)
     bf16_t* su_ = stg + 32 * 128;  // up / du rows
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
+    u32x4 gpre[2][8], upre[2][8];
+    auto fetch = [&](int i, int b) {
       const int mb = mw + 32 * i;
 #pragma unroll
       for (int t = 0; t < 8; ++t) {
@@ -535,9 +572,22 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
           gv = *(const u32x4*)src;
           uv = *(const u32x4*)(src + p.glu_I);
         }
-        *(u32x4*)&sg_[sb(r, cc * 8)] = gv;
-        *(u32x4*)&su_[sb(r, cc * 8)] = uv;
+        gpre[b][t] = gv;
+        upre[b][t] = uv;
       }
+    };
+    fetch(0, 0);
+    if constexpr (TM > 1) fetch(1, 1);
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const int mb = mw + 32 * i;
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const int c = lane + 64 * t, r = c >> 4, cc = c & 15;
+        *(u32x4*)&sg_[sb(r, cc * 8)] = gpre[i & 1][t];
+        *(u32x4*)&su_[sb(r, cc * 8)] = upre[i & 1][t];
+      }
+      if (i + 2 < TM) fetch(i + 2, i & 1);
 #pragma unroll
       for (int j = 0; j < TN; ++j)
 #pragma unroll
@@ -586,12 +636,17 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
             float lo[4], hi[4];
+            // cos and sin of the lane's 4 consecutive angle indices (16-byte loads)
+            f32x4 c4 = {1.f, 1.f, 1.f, 1.f}, s4 = {0.f, 0.f, 0.f, 0.f};
+            if (rot && j + JP < TN) {
+              c4 = *(const f32x4*)(cs + dcol + 8 * q + 4 * lh);
+              s4 = *(const f32x4*)(sn + dcol + 8 * q + 4 * lh);
+            }
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
               const float x1 = acc[i][j][4 * q + e];
               if (rot && j + JP < TN) {
-                const int dc = dcol + 8 * q + 4 * lh + e;
-                const float c = cs[dc], sv = sn[dc];
+                const float c = c4[e], sv = s4[e];
                 const float x2 = acc[i][(j + JP) % TN][4 * q + e];
                 lo[e] = x1 * c - x2 * sv;
                 hi[e] = x2 * c + x1 * sv;
