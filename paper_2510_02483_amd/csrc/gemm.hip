@@ -22,12 +22,14 @@
 // the fragment reads free of bank conflicts):
 //   k-contiguous operand  [256 rows][64 k]  128-byte rows, chunk c of row r at
 //                         slot c ^ ((r/2) % 8); fragments are 16-byte reads.
-//   k-strided operand     [64 k][W cols], W = 256 or 192: k-rows 2j and 2j+1 fill
-//                         the 1 KB block j (at bytes 0 and 2W; for W = 192 the
-//                         last 256 bytes of a block are padding), chunk c of
-//                         row k at slot c ^ ks_swz(k); fragments are two
-//                         transposing 8-byte reads (ds_read_b64_tr_b16), which
-//                         hand each lane 4 consecutive k of one column.
+//   k-strided operand     [64 k][W cols]: for W = 256, k-rows 2j and 2j+1 fill
+//                         the 1 KB block j (at bytes 0 and 512); for W = 192,
+//                         block 8g + b holds k-rows 8b .. 8b+7 of the 64-column
+//                         group g (128 bytes each), so no block carries padding.
+//                         Chunk c of row k sits at slot c ^ ks_swz(k);
+//                         fragments are two transposing 8-byte reads
+//                         (ds_read_b64_tr_b16), which hand each lane 4
+//                         consecutive k of one column.
 // So every layout (forward, input-gradient and weight-gradient products)
 // runs the same matrix-core loop without any explicit transpose.
 //
@@ -87,8 +89,8 @@ LS_DEV void map_tile(int wg, int tiles_m, int tiles_n, int& tm, int& tn) {
 //  - k-strided tiles: a 32-lane transposing read covers 4 consecutive k-rows
 //    (4-aligned) x 64 bytes.  With W = 256 the rows are 512 bytes apart, all at
 //    the same offset of a 256-byte window, and XOR with 4 * (k % 4) puts their
-//    64-byte runs on distinct quarters.  With W = 192 the rows sit at window
-//    offsets 0, 128, 0, 128 (384-byte rows, two per 1 KB block), and XOR with
+//    64-byte runs on distinct quarters.  With W = 192 the rows of a block are
+//    128 bytes apart (window offsets 0, 128, 0, 128), and XOR with
 //    4 * ((k/2) % 2) moves the second pair by 64 bytes.
 LS_DEV int kc_swz(int r) { return (r >> 1) & 7; }
 template <int W>
@@ -98,7 +100,18 @@ LS_DEV int ks_swz(int k) {
 // Element offset of (k-row kk, column col) in a k-strided tile of width W.
 template <int W>
 LS_DEV int ks_off(int kk, int col) {
-  return (kk >> 1) * 512 + (kk & 1) * W + 8 * ((col >> 3) ^ ks_swz<W>(kk)) + (col & 7);
+  if constexpr (W == 256) return (kk >> 1) * 512 + (kk & 1) * W + 8 * ((col >> 3) ^ ks_swz<W>(kk)) + (col & 7);
+  else return ((col >> 6) * 8 + (kk >> 3)) * 512 + (kk & 7) * 64 + 8 * (((col & 63) >> 3) ^ ks_swz<W>(kk)) + (col & 7);
+}
+// Load instructions (1 KB blocks) per wave for a k-strided tile of width W, and
+// the first k-row of block j.
+template <int W>
+constexpr int ks_loads() {
+  return W == 256 ? 8 : 6;
+}
+template <int W>
+LS_DEV int ks_row0(int j) {
+  return W == 256 ? 2 * j : 8 * (j & 7);
 }
 
 LS_DEV float silu_f(float g) { return g * __frcp_rn(1.0f + __expf(-g)); }
@@ -116,15 +129,16 @@ LS_DEV float silu_f(float g) { return g * __frcp_rn(1.0f + __expf(-g)); }
 // tile rows 8j .. 8j+7; lane l writes slot l%8 of row 8j + l/8 with that row's
 // logical chunk c = (l%8) ^ kc_swz(row), i.e. k = k0 + 8c.  The chunk only
 // depends on the parity of j.
-// k-strided operand (rows k, columns m or n): block j holds k-rows 2j and
-// 2j+1 of the tile (W/8 chunks each); lane l < 2 W/8 writes slot l % (W/8) of
-// k-row 2j + l / (W/8) with logical chunk slot ^ ks_swz(k-row); the other lanes
-// of a 192-wide tile load zeros into the padding.
+// k-strided operand (rows k, columns m or n), W = 256: block j holds k-rows 2j
+// and 2j+1 of the tile (32 chunks each); lane l writes slot l % 32 of k-row
+// 2j + l / 32 with logical chunk slot ^ ks_swz(k-row).  W = 192: block 8g + b
+// holds k-rows 8b .. 8b+7 of columns 64g .. 64g+63; lane l writes slot l % 8 of
+// k-row 8b + l / 8.
 template <int NL>
 struct OpLoads {
   i32x4 r;            // resource of the operand (or of B's current k segment)
   uint32_t voff[NL];  // per-lane byte offsets of the loads for the tile at k = 0
-  uint32_t kpos[2];   // k-contiguous: 8c for even / odd blocks; k-strided: l / (W/8)
+  uint32_t kpos[2];   // k-contiguous: 8c for even / odd blocks; k-strided: the lane's k-row in its block
 };
 
 LS_DEV int kc_chunk(int j, int lane) { return (lane & 7) ^ kc_swz(8 * j + (lane >> 3)); }
@@ -147,30 +161,35 @@ LS_DEV void kc_setup(OpLoads<NL>& o, const void* base, int lrow0, int lrows, int
 // placed by the scalar offset (and the resource) of each tile.
 template <int NL, int W>
 LS_DEV void ks_setup(OpLoads<NL>& o, int col0, int cols, int64_t ld, int wave, int lane) {
-  constexpr int CPR = W / 8;  // chunks per k-row
-  const int half = lane / CPR;
+  static_assert(NL == ks_loads<W>(), "one load per 1 KB block");
+  constexpr int CPR = W == 256 ? 32 : 8;  // lanes per k-row
+  const int sub = lane / CPR;              // the lane's k-row within its block
 #pragma unroll
   for (int l = 0; l < NL; ++l) {
-    const int kr = 2 * (wave * NL + l) + half;
-    const int col = col0 + 8 * ((lane % CPR) ^ ks_swz<W>(kr));
-    o.voff[l] = half < 2 && col < cols ? (uint32_t)((int64_t)kr * ld * 2 + col * 2) : OOB;
+    const int j = wave * NL + l;
+    const int kr = ks_row0<W>(j) + sub;
+    const int col = col0 + (W == 256 ? 0 : 64 * (j >> 3)) + 8 * ((lane % CPR) ^ ks_swz<W>(kr));
+    o.voff[l] = col < cols ? (uint32_t)((int64_t)kr * ld * 2 + col * 2) : OOB;
   }
-  o.kpos[0] = half;
-  o.kpos[1] = half;
+  o.kpos[0] = sub;
+  o.kpos[1] = sub;
 }
 
-// Offset of load l of a tile with `kvalid` valid k values (64 for a whole tile).
-template <bool KC, int NL>
+// Offset of load l of a tile with `kvalid` valid k values (64 for a whole tile);
+// W: the width of a k-strided tile (unused for k-contiguous ones).
+template <bool KC, int NL, int W>
 LS_DEV uint32_t load_off(const OpLoads<NL>& o, int l, int kvalid, int wave) {
-  const bool ok = KC ? (int)o.kpos[l & 1] < kvalid : (int)o.kpos[0] < kvalid - 2 * (wave * NL + l);
+  bool ok;
+  if constexpr (KC) ok = (int)o.kpos[l & 1] < kvalid;
+  else ok = (int)o.kpos[0] < kvalid - ks_row0<W>(wave * NL + l);
   return ok ? o.voff[l] : OOB;
 }
 
 // Load l of an operand tile into the LDS block at byte address m0 + l KB
 // (m0: the wave's first block of the stage).
-template <bool KC, int NL>
+template <bool KC, int NL, int W>
 LS_DEV void load_one(const OpLoads<NL>& o, int l, uint32_t soff, int kvalid, uint32_t m0, int wave) {
-  dma1(o.r, load_off<KC>(o, l, kvalid, wave), soff, m0 + 1024u * l);
+  dma1(o.r, load_off<KC, NL, W>(o, l, kvalid, wave), soff, m0 + 1024u * l);
 }
 
 // Fragment of a k-contiguous tile: lane gets row `r` (tile-local), k = 16s + 8*(lane/32) .. +7.
@@ -223,7 +242,7 @@ template <bool AK, bool BKC, int EPI, int BM, int BN>
 __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
   constexpr int WM = BM / 2, WN = BN / 2;  // wave tile
   constexpr int TM = WM / 32, TN = WN / 32;
-  constexpr int NA = AK ? BM / 32 : 8, NB = BKC ? BN / 32 : 8;  // load instructions per wave and tile
+  constexpr int NA = AK ? BM / 32 : ks_loads<BM>(), NB = BKC ? BN / 32 : ks_loads<BN>();  // loads per wave and tile
   constexpr int NL = NA + NB;                                    // loads per wave and tile
   constexpr int NMF = TM * TN;                                   // MFMAs per k-step
   constexpr int NRU = TM + TN;                                   // fragments per k-step
@@ -322,8 +341,8 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
   const uint32_t ma = lds0 + wave * NA * 1024, mb = lds0 + TILE_ELEMS * 2 + wave * NB * 1024;
   // Load q of the tile at the cursor (A loads first) into the stage at byte offset stage_off.
   auto issue = [&](int q, uint32_t stage_off) {
-    if (q < NA) load_one<AK, NA>(la, q, soa, kval, ma + stage_off, wave);
-    else load_one<BKC, NB>(lb, q - NA, sob, kval, mb + stage_off, wave);
+    if (q < NA) load_one<AK, NA, BM>(la, q, soa, kval, ma + stage_off, wave);
+    else load_one<BKC, NB, BN>(lb, q - NA, sob, kval, mb + stage_off, wave);
   };
 
   f32x16 acc[TM][TN];
