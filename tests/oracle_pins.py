@@ -290,11 +290,16 @@ def check_swiglu(ob):
 def torch_block(x, w, c):
     """Independent float64 block built from torch library routines; autograd
     provides every gradient.  RoPE is applied as complex multiplication."""
-    B, S, H = x.shape
-    nq, nkv = c["nq"], c["nkv"]
-    d = w["wq"].shape[0] // nq
     T = {k: torch.tensor(v, requires_grad=True) for k, v in w.items()}
     xt = torch.tensor(x, requires_grad=True)
+    return torch_block_t(xt, T, c), xt, T
+
+
+def torch_block_t(xt, T, c):
+    """The block of torch_block on torch tensors (x [B, S, H], weights T)."""
+    B, S, H = xt.shape
+    nq, nkv = c["nq"], c["nkv"]
+    d = T["wq"].shape[0] // nq
     half = d // 2
     inv = torch.tensor([c["theta"] ** (-2.0 * i / d) for i in range(half)], dtype=torch.float64)
     rot = torch.polar(torch.ones(S, half, dtype=torch.float64),
@@ -313,8 +318,7 @@ def torch_block(x, w, c):
     o = o.transpose(1, 2).reshape(B, S, nq * d)
     x2 = xt + F.linear(o, T["wo"])
     h2 = F.rms_norm(x2, (H,), weight=T["mlp_norm"], eps=c["eps"])
-    y = x2 + F.linear(F.silu(F.linear(h2, T["wg"])) * F.linear(h2, T["wu"]), T["wd"])
-    return y, xt, T
+    return x2 + F.linear(F.silu(F.linear(h2, T["wg"])) * F.linear(h2, T["wu"]), T["wd"])
 
 
 def check_block_vs_torch(ob, c=SMALL, seed=14):
