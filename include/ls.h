@@ -146,6 +146,65 @@ int ls_block_fwd_bwd(const ls_block_cfg* cfg, const ls_bf16* x, const ls_block_w
                      const ls_bf16* dy, ls_bf16* y, ls_bf16* dx, const ls_block_grads* g,
                      int accumulate, void* workspace, size_t workspace_bytes, void* stream);
 
+/* ---- a stack of blocks with a tied embedding and the language-model loss ----
+ *
+ * The models the report trains (Section 2.4; Table 1) put a stack of these
+ * blocks between a token embedding and a final RMSNorm plus LM head, and train
+ * them on the next-token cross-entropy.  With the LM head tied to the embedding
+ * matrix E [vocab, hidden]:
+ *
+ *   x_0 = E[ids];  x_{l+1} = block_l(x_l);  h = RMSNorm(x_L; final_norm);
+ *   z = h E^T;  loss = (1/N) sum over rows t with target[t] >= 0 of
+ *                      (ln sum_v exp z[t, v]) - z[t, target[t]],
+ *
+ * N = number of such rows (loss = 0 when N = 0).  Without explicit targets,
+ * target[b, s] = ids[b, s+1] and the last position of each sequence has none.
+ * The backward pass writes the gradients of E (head part plus embedding
+ * part, summed), of final_norm and of every block's weights. */
+typedef struct {
+  ls_block_cfg block; /* shape of each block; block.batch x block.seq tokens */
+  int32_t n_layers;   /* number of blocks, 0 .. 4096 */
+  int32_t vocab;      /* vocabulary size, a positive multiple of 8; vocab*hidden*4 < 2047 MiB */
+  int32_t recompute;  /* 1: keep only each block's input in the forward pass and
+                         recompute the block's saved state in the backward pass;
+                         0: keep every block's saved state (more workspace) */
+} ls_stack_cfg;
+
+/* embed [vocab, hidden] bf16 (input embedding and LM head); final_norm
+ * [hidden] bf16; layers: HOST array of n_layers ls_block_weights (each holding
+ * device pointers).  Weights of different layers may alias. */
+typedef struct {
+  const ls_bf16* embed;
+  const ls_bf16* final_norm;
+  const ls_block_weights* layers;
+} ls_stack_weights;
+
+/* fp32 gradient accumulators: embed [vocab, hidden], final_norm [hidden],
+ * layers: HOST array of n_layers ls_block_grads.  None may overlap another. */
+typedef struct {
+  float* embed;
+  float* final_norm;
+  const ls_block_grads* layers;
+} ls_stack_grads;
+
+/* Workspace bytes ls_stack_fwd_bwd needs for *cfg. */
+int ls_stack_workspace(const ls_stack_cfg* cfg, size_t* bytes);
+
+/* Forward and backward pass of the whole model for one micro-batch.
+ * ids: [batch*seq] int32 token ids (device).  targets: NULL (next-token
+ * targets from ids) or [batch*seq] int32, -1 = no target.  loss: one fp32
+ * (device).  row_loss: NULL or [batch*seq] fp32, each row's loss (0 without a
+ * target).  Errors reported through the result rather than the status (the
+ * library never reads ids on the host): an id outside [0, vocab) makes its
+ * embedding row NaN, and a target outside [-1, vocab) makes its row's loss
+ * and gradient NaN; neither reads or writes outside any buffer.  The
+ * embedding gradient adds repeated tokens with fp32 atomics, so its low bits
+ * can differ between runs; every other output is deterministic. */
+int ls_stack_fwd_bwd(const ls_stack_cfg* cfg, const int32_t* ids, const int32_t* targets,
+                     const ls_stack_weights* w, float* loss, float* row_loss,
+                     const ls_stack_grads* g, int accumulate, void* workspace,
+                     size_t workspace_bytes, void* stream);
+
 /* ---- single-kernel entry points (used for per-kernel parity) ---------------- */
 
 /* Causal attention core on a packed projection buffer.
@@ -190,6 +249,27 @@ int ls_gemm_nn(int64_t M, int64_t N, int64_t K, const ls_bf16* A, const ls_bf16*
 int ls_gemm_tn(int64_t M, int64_t N, int64_t K, const ls_bf16* A, const ls_bf16* B,
                float* C, int accumulate, void* stream);
 
+/* Softmax cross-entropy over rows of bf16 logits [tokens, vocab], in place:
+ * row_loss[t] = ln sum_v exp z[t,v] - z[t, target[t]] (0 when target[t] = -1),
+ * loss = sum(row_loss) / max(N, 1), and logits are overwritten with the
+ * gradient of loss, (softmax(z[t]) - onehot(target[t])) / max(N, 1) (zero rows
+ * without a target).  targets: NULL (next token of ids within sequences of
+ * `seq` tokens; tokens must be a multiple of seq) or [tokens] int32.  A target
+ * outside [-1, vocab) makes its row NaN.  workspace: at least
+ * ls_cross_entropy_workspace(tokens) bytes. */
+size_t ls_cross_entropy_workspace(int64_t tokens);
+int ls_cross_entropy(int64_t tokens, int32_t seq, int32_t vocab, ls_bf16* logits,
+                     const int32_t* ids, const int32_t* targets, float* loss, float* row_loss,
+                     void* workspace, size_t workspace_bytes, void* stream);
+
+/* Token embedding rows: x[t] = embed[ids[t]] ([tokens, hidden] bf16; an id
+ * outside [0, vocab) gives a NaN row), and its backward, which ADDS dx[t] into
+ * d_embed[ids[t]] (fp32; ids outside [0, vocab) skipped). */
+int ls_embed_fwd(int64_t tokens, int32_t hidden, int32_t vocab, const int32_t* ids,
+                 const ls_bf16* embed, ls_bf16* x, void* stream);
+int ls_embed_bwd(int64_t tokens, int32_t hidden, int32_t vocab, const int32_t* ids,
+                 const ls_bf16* dx, float* d_embed, void* stream);
+
 /* Tile shape of the matrix products (tuning and testing).  By default every
  * product launch picks its workgroup tile (256 or 192 rows x 256 or 192
  * columns, where its epilogue allows) to minimise waves of workgroups times
@@ -206,7 +286,9 @@ int ls_gemm_tile_override(int32_t bm, int32_t bn);
  * equals `label` (labels: "rmsnorm fwd", "qkv projection", "attention fwd",
  * "output projection", "gate/up projection", "down projection", "dact",
  * "dWd", "dh2", "dWg/dWu", "rmsnorm bwd", "dO", "dWo", "attention bwd",
- * "dh1", "dWqkv"), creating up to max_launches event pairs up front;
+ * "dh1", "dWqkv", and in ls_stack_fwd_bwd also "embedding fwd", "targets",
+ * "logits", "cross-entropy", "dh head", "dE head", "loss", "embedding bwd"),
+ * creating up to max_launches event pairs up front;
  * later calls record into them without allocating.  ls_timing_end waits for
  * the recorded events, writes the number of recorded launches and their mean
  * duration in milliseconds, disarms recording and releases the events.

@@ -58,3 +58,30 @@ B30 = BlockConfig("30b", 3, batch=2, seq=2048, hidden=6656, n_q_heads=52, n_kv_h
                   head_dim=128, intermediate=17920, rope_theta=1e4)
 
 PRESETS = {c.name: c for c in (TINY, B3, B3_8K, B30)}
+
+
+@dataclass(frozen=True)
+class StackConfig:
+    """A stack of identical blocks between a tied token embedding and a final
+    RMSNorm + LM head, trained on next-token cross-entropy (Section 2.4)."""
+    name: str
+    block: BlockConfig   # shape of every block; block.cfg_id seeds the inputs
+    n_layers: int
+    vocab: int
+    recompute: bool = True  # keep only block inputs; recompute each block in the backward
+
+    @property
+    def tokens(self) -> int:
+        return self.block.tokens
+
+    def with_(self, **kw) -> "StackConfig":
+        return replace(self, **kw)
+
+
+# Small stack: parity case for the fp64 oracle (a few seconds).
+TINY_STACK = StackConfig("tiny_stack", TINY.with_(name="tiny_stack_block", cfg_id=10, batch=2, seq=64),
+                         n_layers=2, vocab=1000)
+# Llama-3.2-3B-shaped model: 28 blocks, vocabulary 128256, micro-batch 4 x 2048.
+STACK_3B = StackConfig("3b_stack", B3.with_(name="3b_stack_block", cfg_id=4), n_layers=28, vocab=128256)
+
+STACK_PRESETS = {c.name: c for c in (TINY_STACK, STACK_3B)}

@@ -568,6 +568,62 @@ int run_mlp_bwd(const ls_block_cfg& cfg, const Dims& m, const bf16_t* x2, const 
   return LS_OK;
 }
 
+// ---- the stack of blocks with a tied embedding, LM head and cross-entropy ------------
+
+int check_stack_cfg(const ls_stack_cfg* c) {
+  if (!c) return fail(LS_ERR_NULL, "cfg is NULL");
+  if (int e = check_cfg(&c->block)) return e;
+  if (c->n_layers < 0 || c->n_layers > 4096) return fail(LS_ERR_SHAPE, "n_layers %d out of range [0, 4096]", c->n_layers);
+  if (c->vocab <= 0 || c->vocab % 8 != 0) return fail(LS_ERR_SHAPE, "vocab (%d) must be a positive multiple of 8", c->vocab);
+  if (c->recompute != 0 && c->recompute != 1) return fail(LS_ERR_SHAPE, "recompute must be 0 or 1");
+  if ((int64_t)c->vocab * c->block.hidden * 4 >= kMaxBytes)
+    return fail(LS_ERR_SHAPE, "vocab x hidden fp32 gradient reaches 2047 MiB");
+  return LS_OK;
+}
+
+// Token rows per logits chunk: the [rows, vocab] bf16 logits of one chunk stay
+// below the 2047 MiB limit of one matrix-product operand.
+int64_t logits_rows(const ls_stack_cfg& c) {
+  const Dims m = dims_of(c.block);
+  int64_t per = (kMaxBytes - 1) / ((int64_t)c.vocab * 2);
+  if (per >= 256) per &= ~(int64_t)255;
+  return std::min<int64_t>(m.T, per);
+}
+
+struct StackWs {
+  size_t tg, counts, rows, xs, hf, rf, logits, dh, dxa, dxb, ysink, partial, sets, set_stride, dx2, scratch, total;
+  size_t asv, msv, x2;  // offsets inside one set
+};
+StackWs stack_ws_layout(const ls_stack_cfg& c) {
+  const Dims m = dims_of(c.block);
+  const size_t act = (size_t)(m.T * m.H * 2);
+  Carver k;
+  StackWs w;
+  w.tg = k.take(m.T * 4);
+  w.counts = k.take(16);
+  w.rows = k.take(m.T * 4);
+  w.xs = k.take(act * (size_t)(c.n_layers + 1));
+  w.hf = k.take(act);
+  w.rf = k.take(m.T * 4);
+  w.logits = k.take((size_t)logits_rows(c) * c.vocab * 2);
+  w.dh = k.take(act);
+  w.dxa = k.take(act);
+  w.dxb = k.take(act);
+  w.ysink = k.take(c.recompute ? act : 0);
+  w.partial = k.take(norm_partial_bytes(m));
+  w.dx2 = k.take(act);
+  w.scratch = k.take(std::max(attn_ws_layout(m).total, mlp_ws_layout(m).total));
+  Carver one;
+  w.asv = one.take(attn_saved_layout(m).total);
+  w.msv = one.take(mlp_saved_layout(m).total);
+  w.x2 = one.take(act);
+  w.set_stride = one.off;
+  const int nsets = c.recompute ? (c.n_layers > 0 ? 1 : 0) : c.n_layers;
+  w.sets = k.take(w.set_stride * (size_t)nsets);
+  w.total = k.off;
+  return w;
+}
+
 }  // namespace
 
 extern "C" {
@@ -883,6 +939,199 @@ int ls_gemm_tn(int64_t M, int64_t N, int64_t K, const ls_bf16* A, const ls_bf16*
   g.ldf = N;
   g.accumulate = accumulate != 0;
   LS_HIP(ls::gemm(g, (hipStream_t)stream), "gemm_tn");
+  return LS_OK;
+}
+
+
+int ls_stack_workspace(const ls_stack_cfg* cfg, size_t* bytes) {
+  if (int e = check_stack_cfg(cfg)) return e;
+  if (!bytes) return fail(LS_ERR_NULL, "bytes is NULL");
+  *bytes = stack_ws_layout(*cfg).total;
+  return LS_OK;
+}
+
+int ls_stack_fwd_bwd(const ls_stack_cfg* cfg, const int32_t* ids, const int32_t* targets, const ls_stack_weights* w,
+                     float* loss, float* row_loss, const ls_stack_grads* g, int accumulate, void* workspace,
+                     size_t workspace_bytes, void* stream) {
+  if (int e = check_stack_cfg(cfg)) return e;
+  if (!w || !g) return fail(LS_ERR_NULL, "weights or grads is NULL");
+  const int L = cfg->n_layers;
+  if (L > 0 && (!w->layers || !g->layers)) return fail(LS_ERR_NULL, "layer weights or grads array is NULL");
+  const Dims m = dims_of(cfg->block);
+  const int64_t V = cfg->vocab;
+  const StackWs wl = stack_ws_layout(*cfg);
+  std::vector<Range> in{{ids, (size_t)m.T * 4, "ids"},
+                        {w->embed, (size_t)(V * m.H * 2), "w.embed"},
+                        {w->final_norm, (size_t)m.H * 2, "w.final_norm"}};
+  if (targets) in.push_back({targets, (size_t)m.T * 4, "targets"});
+  std::vector<Range> out{{loss, 4, "loss"},
+                         {g->embed, (size_t)(V * m.H * 4), "g.embed"},
+                         {g->final_norm, (size_t)m.H * 4, "g.final_norm"},
+                         {workspace, workspace_bytes, "workspace"}};
+  if (row_loss) out.push_back({row_loss, (size_t)m.T * 4, "row_loss"});
+  for (int l = 0; l < L; ++l) {
+    weight_ranges(m, &w->layers[l], true, true, in);
+    grad_ranges(m, &g->layers[l], true, true, out);
+  }
+  if (int e = check_ranges(in, out)) return e;
+  if (workspace_bytes < wl.total) return fail(LS_ERR_WORKSPACE, "workspace %zu < %zu bytes", workspace_bytes, wl.total);
+
+  const hipStream_t st = (hipStream_t)stream;
+  const ls_block_cfg& bc = cfg->block;
+  const int acc = accumulate != 0;
+  const size_t act = (size_t)(m.T * m.H * 2);
+  const bf16_t* E = (const bf16_t*)w->embed;
+  auto xs = [&](int l) { return at<bf16_t>(workspace, wl.xs + act * (size_t)l); };
+  auto set = [&](int l) { return at<char>(workspace, wl.sets + wl.set_stride * (size_t)(cfg->recompute ? 0 : l)); };
+  int32_t* tg = at<int32_t>(workspace, wl.tg);
+  int* counts = at<int>(workspace, wl.counts);
+  float* rows = row_loss ? row_loss : at<float>(workspace, wl.rows);
+  bf16_t* hf = at<bf16_t>(workspace, wl.hf);
+  float* rf = at<float>(workspace, wl.rf);
+  bf16_t* logits = at<bf16_t>(workspace, wl.logits);
+  bf16_t* dh = at<bf16_t>(workspace, wl.dh);
+  bf16_t* dxa = at<bf16_t>(workspace, wl.dxa);
+  bf16_t* dxb = at<bf16_t>(workspace, wl.dxb);
+  bf16_t* dx2 = at<bf16_t>(workspace, wl.dx2);
+  void* scratch = at<char>(workspace, wl.scratch);
+
+  // forward: embedding, blocks (keeping every block's input), final norm
+  LS_STEP("embedding fwd", st, ls::embed_fwd(m.T, (int)m.H, (int)V, ids, E, xs(0), st));
+  for (int l = 0; l < L; ++l) {
+    char* sv = set(l);
+    if (int e = run_attn_fwd(bc, m, xs(l), &w->layers[l], at<bf16_t>(sv, wl.x2), sv + wl.asv, scratch, st)) return e;
+    if (int e = run_mlp_fwd(bc, m, at<bf16_t>(sv, wl.x2), &w->layers[l], xs(l + 1), sv + wl.msv, st)) return e;
+  }
+  LS_STEP("rmsnorm fwd", st,
+          ls::rmsnorm_fwd(m.T, (int)m.H, bc.rms_eps, xs(L), (const bf16_t*)w->final_norm, hf, rf, st));
+
+  // LM head and cross-entropy, chunk by chunk of token rows
+  LS_STEP("targets", st, ls::ce_targets(m.T, (int)m.S, (int)V, ids, targets, tg, counts, st));
+  const int64_t tc_max = logits_rows(*cfg);
+  for (int64_t t0 = 0; t0 < m.T; t0 += tc_max) {
+    const int64_t tc = std::min(tc_max, m.T - t0);
+    {  // logits = h E^T
+      ls::GemmArgs a;
+      a.M = (int)tc;
+      a.N = (int)V;
+      a.K = (int)m.H;
+      a.A = hf + t0 * m.H;
+      a.lda = m.H;
+      a.B[0] = E;
+      a.ldb = m.H;
+      a.epi = ls::EPI_BF16;
+      a.C = logits;
+      a.ldc = V;
+      LS_STEP("logits", st, ls::gemm(a, st));
+    }
+    LS_STEP("cross-entropy", st, ls::ce_rows(tc, (int)V, logits, tg + t0, counts, rows + t0, st));
+    {  // dh = dz E
+      ls::GemmArgs a;
+      a.M = (int)tc;
+      a.N = (int)m.H;
+      a.K = (int)V;
+      a.A = logits;
+      a.lda = V;
+      a.B[0] = E;
+      a.ldb = m.H;
+      a.b_kcontig = false;
+      a.epi = ls::EPI_BF16;
+      a.C = dh + t0 * m.H;
+      a.ldc = m.H;
+      LS_STEP("dh head", st, ls::gemm(a, st));
+    }
+    {  // dE (+)= dz^T h
+      ls::GemmArgs a;
+      a.M = (int)V;
+      a.N = (int)m.H;
+      a.K = (int)tc;
+      a.A = logits;
+      a.lda = V;
+      a.a_kcontig = false;
+      a.B[0] = hf + t0 * m.H;
+      a.ldb = m.H;
+      a.b_kcontig = false;
+      a.epi = ls::EPI_F32;
+      a.F[0] = g->embed;
+      a.ldf = m.H;
+      a.accumulate = (t0 > 0) || acc;
+      LS_STEP("dE head", st, ls::gemm(a, st));
+    }
+  }
+  LS_STEP("loss", st, ls::ce_loss(m.T, rows, counts, loss, st));
+
+  // backward through the final norm and the blocks, recomputing each block's
+  // saved state from its input when asked to
+  bf16_t* dcur = dxa;
+  bf16_t* dnext = dxb;
+  LS_STEP("rmsnorm bwd", st,
+          ls::rmsnorm_bwd(m.T, (int)m.H, xs(L), (const bf16_t*)w->final_norm, rf, dh, nullptr, dcur, g->final_norm,
+                          acc, at<float>(workspace, wl.partial), st));
+  for (int l = L - 1; l >= 0; --l) {
+    char* sv = set(l);
+    bf16_t* x2 = at<bf16_t>(sv, wl.x2);
+    if (cfg->recompute) {
+      if (int e = run_attn_fwd(bc, m, xs(l), &w->layers[l], x2, sv + wl.asv, scratch, st)) return e;
+      if (int e = run_mlp_fwd(bc, m, x2, &w->layers[l], at<bf16_t>(workspace, wl.ysink), sv + wl.msv, st)) return e;
+    }
+    if (int e = run_mlp_bwd(bc, m, x2, &w->layers[l], sv + wl.msv, dcur, dx2, &g->layers[l], acc, scratch, st))
+      return e;
+    if (int e = run_attn_bwd(bc, m, xs(l), &w->layers[l], sv + wl.asv, dx2, dnext, &g->layers[l], acc, scratch, st))
+      return e;
+    std::swap(dcur, dnext);
+  }
+  LS_STEP("embedding bwd", st, ls::embed_bwd(m.T, (int)m.H, (int)V, ids, dcur, g->embed, st));
+  return LS_OK;
+}
+
+size_t ls_cross_entropy_workspace(int64_t tokens) { return up256((size_t)(tokens > 0 ? tokens : 0) * 4) + 256; }
+
+int ls_cross_entropy(int64_t tokens, int32_t seq, int32_t vocab, ls_bf16* logits, const int32_t* ids,
+                     const int32_t* targets, float* loss, float* row_loss, void* workspace, size_t workspace_bytes,
+                     void* stream) {
+  if (tokens <= 0 || seq <= 0 || vocab <= 0 || vocab % 8 != 0)
+    return fail(LS_ERR_SHAPE, "tokens, seq must be positive and vocab a positive multiple of 8");
+  if (tokens >= ((int64_t)1 << 31)) return fail(LS_ERR_SHAPE, "tokens (%lld) reaches 2^31", (long long)tokens);
+  if (!targets && tokens % seq != 0) return fail(LS_ERR_SHAPE, "tokens (%lld) is not a multiple of seq (%d)",
+                                                 (long long)tokens, seq);
+  std::vector<Range> in{{ids, (size_t)tokens * 4, "ids"}};
+  if (targets) in.push_back({targets, (size_t)tokens * 4, "targets"});
+  std::vector<Range> out{{logits, (size_t)(tokens * vocab * 2), "logits"},
+                         {loss, 4, "loss"},
+                         {row_loss, (size_t)tokens * 4, "row_loss"},
+                         {workspace, workspace_bytes, "workspace"}};
+  if (int e = check_ranges(in, out)) return e;
+  if (workspace_bytes < ls_cross_entropy_workspace(tokens))
+    return fail(LS_ERR_WORKSPACE, "workspace %zu < %zu bytes", workspace_bytes, ls_cross_entropy_workspace(tokens));
+  const hipStream_t st = (hipStream_t)stream;
+  int32_t* tg = (int32_t*)workspace;
+  int* counts = at<int>(workspace, up256((size_t)tokens * 4));
+  LS_HIP(ls::ce_targets(tokens, seq, vocab, ids, targets, tg, counts, st), "targets");
+  LS_HIP(ls::ce_rows(tokens, vocab, (bf16_t*)logits, tg, counts, row_loss, st), "cross-entropy");
+  LS_HIP(ls::ce_loss(tokens, row_loss, counts, loss, st), "loss");
+  return LS_OK;
+}
+
+int ls_embed_fwd(int64_t tokens, int32_t hidden, int32_t vocab, const int32_t* ids, const ls_bf16* embed, ls_bf16* x,
+                 void* stream) {
+  if (tokens <= 0 || hidden <= 0 || hidden % 8 != 0 || vocab <= 0)
+    return fail(LS_ERR_SHAPE, "tokens, vocab must be positive and hidden a positive multiple of 8");
+  std::vector<Range> in{{ids, (size_t)tokens * 4, "ids"}, {embed, (size_t)vocab * hidden * 2, "embed"}};
+  std::vector<Range> out{{x, (size_t)(tokens * hidden * 2), "x"}};
+  if (int e = check_ranges(in, out)) return e;
+  LS_HIP(ls::embed_fwd(tokens, hidden, vocab, ids, (const bf16_t*)embed, (bf16_t*)x, (hipStream_t)stream),
+         "embedding fwd");
+  return LS_OK;
+}
+
+int ls_embed_bwd(int64_t tokens, int32_t hidden, int32_t vocab, const int32_t* ids, const ls_bf16* dx, float* d_embed,
+                 void* stream) {
+  if (tokens <= 0 || hidden <= 0 || hidden % 8 != 0 || vocab <= 0)
+    return fail(LS_ERR_SHAPE, "tokens, vocab must be positive and hidden a positive multiple of 8");
+  std::vector<Range> in{{ids, (size_t)tokens * 4, "ids"}, {dx, (size_t)(tokens * hidden * 2), "dx"}};
+  std::vector<Range> out{{d_embed, (size_t)vocab * hidden * 4, "d_embed"}};
+  if (int e = check_ranges(in, out)) return e;
+  LS_HIP(ls::embed_bwd(tokens, hidden, vocab, ids, (const bf16_t*)dx, d_embed, (hipStream_t)stream), "embedding bwd");
   return LS_OK;
 }
 

@@ -82,4 +82,19 @@ size_t attn_bwd_workspace(const AttnShape& sh);
 hipError_t attn_bwd(const AttnShape& sh, const bf16_t* qkv, const bf16_t* o, const float* lse,
                     const bf16_t* dout, bf16_t* dqkv, const float* rope_cs, void* ws, hipStream_t s);
 
+// ---- token embedding and cross-entropy ------------------------------------------
+// x[t] = E[ids[t]] ([T, H] bf16); an id outside [0, V) gives a NaN row.
+hipError_t embed_fwd(int64_t T, int H, int V, const int32_t* ids, const bf16_t* E, bf16_t* x, hipStream_t s);
+// dE[ids[t]] += dx[t] (fp32 atomics; ids outside [0, V) skipped).
+hipError_t embed_bwd(int64_t T, int H, int V, const int32_t* ids, const bf16_t* dx, float* dE, hipStream_t s);
+// tg[t] = targets[t], or (targets null) ids[t+1] within a sequence of S tokens
+// and -1 at its last position; counts[0] = rows with a target in [0, V).
+hipError_t ce_targets(int64_t T, int S, int V, const int32_t* ids, const int32_t* targets, int32_t* tg, int* counts,
+                      hipStream_t s);
+// Per row of z [rows, V] bf16: row_loss = lse - z[tg]; z <- (softmax - onehot) / max(counts[0], 1).
+hipError_t ce_rows(int64_t rows, int V, bf16_t* z, const int32_t* tg, const int* counts, float* row_loss,
+                   hipStream_t s);
+// loss = sum(row_loss[0 .. T)) / max(counts[0], 1).
+hipError_t ce_loss(int64_t T, const float* row_loss, const int* counts, float* loss, hipStream_t s);
+
 }  // namespace ls

@@ -7,7 +7,7 @@ S(S+1)/2 query-key pairs that the mask keeps; the non-causal convention
 """
 from __future__ import annotations
 
-from .configs import BlockConfig
+from .configs import BlockConfig, StackConfig
 
 
 def block_params(hidden: int, dq: int, dkv: int, inter: int) -> int:
@@ -45,3 +45,15 @@ def training_flops_per_token(n_layers: int, hidden: int, n_heads: int, n_kv_head
     d = hidden // n_heads
     n = n_layers * block_params(hidden, n_heads * d, n_kv_heads * d, inter) + vocab * hidden
     return 6.0 * n + 12.0 * n_layers * hidden * seq
+
+
+def lm_head_fwd_bwd_flops(tokens: int, hidden: int, vocab: int) -> float:
+    """Logits h E^T, and in the backward dh = dz E and dE = dz^T h."""
+    return 3.0 * 2.0 * tokens * hidden * vocab
+
+
+def stack_fwd_bwd_flops(sc: StackConfig, causal: bool = True) -> float:
+    """Model FLOPs of the stack's forward plus backward pass: every block and
+    the tied LM head (recomputation in the backward pass is not counted)."""
+    return sc.n_layers * block_fwd_bwd_flops(sc.block, causal) + \
+        lm_head_fwd_bwd_flops(sc.tokens, sc.block.hidden, sc.vocab)

@@ -11,7 +11,7 @@ import os
 
 import torch
 
-from .configs import BlockConfig
+from .configs import BlockConfig, StackConfig
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libls.so")
@@ -47,6 +47,21 @@ class LsSizes(ctypes.Structure):
                 ("block_workspace", ctypes.c_size_t)]
 
 
+class LsStackCfg(ctypes.Structure):
+    _fields_ = [("block", LsBlockCfg), ("n_layers", ctypes.c_int32), ("vocab", ctypes.c_int32),
+                ("recompute", ctypes.c_int32)]
+
+
+class LsStackWeights(ctypes.Structure):
+    _fields_ = [("embed", ctypes.c_void_p), ("final_norm", ctypes.c_void_p),
+                ("layers", ctypes.POINTER(LsBlockWeights))]
+
+
+class LsStackGrads(ctypes.Structure):
+    _fields_ = [("embed", ctypes.c_void_p), ("final_norm", ctypes.c_void_p),
+                ("layers", ctypes.POINTER(LsBlockGrads))]
+
+
 _lib = None
 _P = ctypes.c_void_p
 _PROTOS = {
@@ -70,6 +85,13 @@ _PROTOS = {
     "ls_gemm_nn": (ctypes.c_int, [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, _P, _P, _P, _P]),
     "ls_gemm_tn": (ctypes.c_int, [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, _P, _P, _P, ctypes.c_int, _P]),
     "ls_gemm_tile_override": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32]),
+    "ls_stack_workspace": (ctypes.c_int, [_P, _P]),
+    "ls_stack_fwd_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, ctypes.c_int, _P, ctypes.c_size_t, _P]),
+    "ls_cross_entropy_workspace": (ctypes.c_size_t, [ctypes.c_int64]),
+    "ls_cross_entropy": (ctypes.c_int, [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _P, _P, _P, _P, _P, _P,
+                                        ctypes.c_size_t, _P]),
+    "ls_embed_fwd": (ctypes.c_int, [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _P, _P, _P, _P]),
+    "ls_embed_bwd": (ctypes.c_int, [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _P, _P, _P, _P]),
     "ls_timing_begin": (ctypes.c_int, [ctypes.c_char_p, ctypes.c_int]),
     "ls_timing_end": (ctypes.c_int, [_P, _P]),
 }
@@ -218,6 +240,53 @@ def ls_gemm_tn(A, B, C, accumulate=False, stream=None):
     _check(lib().ls_gemm_tn(M, N, K, _p(A), _p(B), _p(C), int(accumulate), _stream(stream)), "ls_gemm_tn")
 
 
+def make_stack_cfg(sc: StackConfig) -> LsStackCfg:
+    return LsStackCfg(make_cfg(sc.block), sc.n_layers, sc.vocab, int(sc.recompute))
+
+
+def ls_stack_workspace(sc: StackConfig) -> int:
+    cfg = make_stack_cfg(sc)
+    n = ctypes.c_size_t(0)
+    _check(lib().ls_stack_workspace(ctypes.byref(cfg), ctypes.byref(n)), "ls_stack_workspace")
+    return n.value
+
+
+def ls_stack_fwd_bwd(sc: StackConfig, ids, targets, embed, final_norm, layers, loss, row_loss, d_embed,
+                     d_final_norm, d_layers, accumulate, workspace, stream=None):
+    """layers / d_layers: lists of per-block weight / gradient dicts (device tensors)."""
+    cfg = make_stack_cfg(sc)
+    L = sc.n_layers
+    lw = (LsBlockWeights * max(L, 1))(*[make_weights(w) for w in layers])
+    lg = (LsBlockGrads * max(L, 1))(*[make_grads(g) for g in d_layers])
+    w = LsStackWeights(embed.data_ptr(), final_norm.data_ptr(), lw)
+    g = LsStackGrads(d_embed.data_ptr(), d_final_norm.data_ptr(), lg)
+    _check(lib().ls_stack_fwd_bwd(ctypes.byref(cfg), _p(ids), _p(targets), ctypes.byref(w), _p(loss), _p(row_loss),
+                                  ctypes.byref(g), int(accumulate), _p(workspace),
+                                  workspace.numel() * workspace.element_size(), _stream(stream)), "ls_stack_fwd_bwd")
+
+
+def ls_cross_entropy_workspace(tokens: int) -> int:
+    return lib().ls_cross_entropy_workspace(int(tokens))
+
+
+def ls_cross_entropy(logits, seq, ids, targets, loss, row_loss, workspace, stream=None):
+    """logits [tokens, vocab] bf16 is overwritten with the gradient of the loss."""
+    T, V = logits.shape
+    _check(lib().ls_cross_entropy(T, int(seq), V, _p(logits), _p(ids), _p(targets), _p(loss), _p(row_loss),
+                                  _p(workspace), workspace.numel() * workspace.element_size(), _stream(stream)),
+           "ls_cross_entropy")
+
+
+def ls_embed_fwd(ids, embed, x, stream=None):
+    V, H = embed.shape
+    _check(lib().ls_embed_fwd(ids.numel(), H, V, _p(ids), _p(embed), _p(x), _stream(stream)), "ls_embed_fwd")
+
+
+def ls_embed_bwd(ids, dx, d_embed, stream=None):
+    V, H = d_embed.shape
+    _check(lib().ls_embed_bwd(ids.numel(), H, V, _p(ids), _p(dx), _p(d_embed), _stream(stream)), "ls_embed_bwd")
+
+
 def ls_timing_begin(label: str, max_launches: int):
     _check(lib().ls_timing_begin(label.encode(), int(max_launches)), "ls_timing_begin")
 
@@ -253,3 +322,31 @@ class Block:
     def step(self, accumulate=False, stream=None):
         ls_block_fwd_bwd(self.cfg, self.x, self.w, self.dy, self.y, self.dx, self.grads, accumulate,
                          self.workspace, stream)
+
+
+class Stack:
+    """Device buffers for one stack configuration plus a call of ls_stack_fwd_bwd.
+
+    ``host`` is the dict of inputs.make_stack_inputs (CPU or device tensors);
+    everything is moved to the device once.  Gradients are fp32."""
+
+    def __init__(self, sc: StackConfig, host: dict, device="cuda", targets=None):
+        self.cfg = sc
+        dev = torch.device(device)
+        self.ids = host["ids"].to(dev).reshape(-1).contiguous()
+        self.targets = None if targets is None else targets.to(dev).reshape(-1).contiguous()
+        self.embed = host["embed"].to(dev).contiguous()
+        self.final_norm = host["final_norm"].to(dev).contiguous()
+        self.layers = [{n: l[n].to(dev).contiguous() for n in WEIGHTS} for l in host["layers"]]
+        self.d_embed = torch.zeros(self.embed.shape, dtype=torch.float32, device=dev)
+        self.d_final_norm = torch.zeros(self.final_norm.shape, dtype=torch.float32, device=dev)
+        self.d_layers = [{n: torch.zeros(w[n].shape, dtype=torch.float32, device=dev) for n in WEIGHTS}
+                         for w in self.layers]
+        self.loss = torch.zeros(1, dtype=torch.float32, device=dev)
+        self.row_loss = torch.zeros(sc.tokens, dtype=torch.float32, device=dev)
+        self.workspace = torch.empty(ls_stack_workspace(sc), dtype=torch.uint8, device=dev)
+
+    def step(self, accumulate=False, stream=None):
+        ls_stack_fwd_bwd(self.cfg, self.ids, self.targets, self.embed, self.final_norm, self.layers, self.loss,
+                         self.row_loss, self.d_embed, self.d_final_norm, self.d_layers, accumulate, self.workspace,
+                         stream)

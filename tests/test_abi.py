@@ -128,3 +128,82 @@ def test_gemm_tile_override_arguments():
     assert lib.ls_gemm_tile_override(256, 128) == 2
     assert lib.ls_gemm_tile_override(192, 256) == 0
     assert lib.ls_gemm_tile_override(0, 0) == 0
+
+
+def _stack_args(sc, L_=None):
+    """Fake, disjoint, aligned device addresses for every stack argument (the
+    checks run before any HIP call, so nothing is dereferenced)."""
+    n = sc.n_layers if L_ is None else L_
+    lw = (L.LsBlockWeights * max(n, 1))(*[_fake_weights(sc.block, base=(1 << 36) + l * (1 << 34)) for l in range(n)])
+    lg = (L.LsBlockGrads * max(n, 1))(*[_fake_grads(sc.block, base=(1 << 44) + l * (1 << 34)) for l in range(n)])
+    w = L.LsStackWeights(1 << 52, (1 << 52) + (1 << 40), lw)
+    g = L.LsStackGrads(1 << 53, (1 << 53) + (1 << 40), lg)
+    return w, g
+
+
+def test_stack_workspace_and_config_checks():
+    sc = configs.TINY_STACK
+    need = L.ls_stack_workspace(sc)
+    c, T, H, V = sc.block, sc.tokens, sc.block.hidden, sc.vocab
+    # block inputs of every layer, the logits, one block's saved state
+    assert need >= 2 * T * H * (sc.n_layers + 1) + 2 * T * V + L.ls_query_sizes(c)["attn_saved"]
+    assert L.ls_stack_workspace(sc.with_(recompute=False)) > need
+    assert L.ls_stack_workspace(sc.with_(n_layers=0)) < need
+    for bad, status in [(dict(vocab=1001), 2), (dict(vocab=0), 2), (dict(n_layers=-1), 2),
+                        (dict(vocab=1 << 20, block=c.with_(hidden=512)), 2),
+                        (dict(block=c.with_(head_dim=96)), 3)]:
+        with pytest.raises(L.LsError) as e:
+            L.ls_stack_workspace(sc.with_(**bad))
+        assert e.value.status == status, bad
+    lib = L.lib()
+    cfg = L.make_stack_cfg(sc)
+    cfg.recompute = 2
+    n = ctypes.c_size_t(0)
+    assert lib.ls_stack_workspace(ctypes.byref(cfg), ctypes.byref(n)) == 2
+    assert lib.ls_stack_workspace(None, ctypes.byref(n)) == 1
+
+
+def test_stack_argument_checks():
+    lib = L.lib()
+    sc = configs.TINY_STACK
+    cfg = L.make_stack_cfg(sc)
+    need = L.ls_stack_workspace(sc)
+    V = ctypes.c_void_p
+    ids, tgt, loss, rows, ws = (1 << 32), (1 << 33), (1 << 34), (1 << 35), (1 << 50)
+    w, g = _stack_args(sc)
+    call = lambda ids_, w_, g_, loss_, ws_, n: lib.ls_stack_fwd_bwd(  # noqa: E731
+        ctypes.byref(cfg), V(ids_), None, ctypes.byref(w_), V(loss_), V(rows), ctypes.byref(g_), 0, V(ws_), n, None)
+    assert call(None, w, g, loss, ws, need) == 1
+    assert call(ids, w, g, None, ws, need) == 1
+    assert call(ids + 4, w, g, loss, ws, need) == 4
+    assert call(ids, w, g, ids, ws, need) == 5                 # loss aliases ids
+    assert call(ids, w, g, loss, ws, need - 256) == 6
+    g2 = L.LsStackGrads(g.embed, g.final_norm, g.layers)
+    g2.embed = w.embed                                         # gradient over the embedding
+    assert call(ids, w, g2, loss, ws, need) == 5
+    w0, g0 = _stack_args(sc)
+    g0.layers[1].wq = g0.layers[0].wq                          # two layers share a gradient buffer
+    assert call(ids, w0, g0, loss, ws, need) == 5
+    w1, g1 = _stack_args(sc)
+    w1.layers[1].wq = w1.layers[0].wq                          # tied layer weights are allowed
+    assert lib.ls_stack_fwd_bwd(ctypes.byref(cfg), V(ids), V(tgt), ctypes.byref(w1), V(loss), None,
+                                ctypes.byref(g1), 0, V(ws), need - 1, None) == 6
+    w3 = L.LsStackWeights(w.embed, w.final_norm, None)
+    assert call(ids, w3, g, loss, ws, need) == 1
+
+
+def test_cross_entropy_and_embedding_argument_checks():
+    lib = L.lib()
+    V = ctypes.c_void_p
+    need = lib.ls_cross_entropy_workspace(100)
+    assert need >= 400
+    z, ids, loss, rows, ws = (1 << 32), (1 << 33), (1 << 34), (1 << 35), (1 << 36)
+    ce = lambda T, S, Vv, n, z_=z: lib.ls_cross_entropy(T, S, Vv, V(z_), V(ids), None, V(loss), V(rows),  # noqa
+                                                         V(ws), n, None)
+    assert ce(100, 10, 1001, need) == 2   # vocab not a multiple of 8
+    assert ce(100, 7, 1000, need) == 2    # next-token targets need whole sequences
+    assert ce(100, 10, 1000, need - 4) == 6
+    assert ce(100, 10, 1000, need, z_=ids) == 5
+    assert lib.ls_embed_fwd(10, 12, 100, V(ids), V(z), V(rows), None) == 2
+    assert lib.ls_embed_fwd(10, 16, 100, V(ids), V(z), V(ids), None) == 5
+    assert lib.ls_embed_bwd(10, 16, 100, None, V(z), V(rows), None) == 1
