@@ -1,6 +1,7 @@
 """Benchmark: one Llama-style decoder block, forward + backward, on one MI355X.
 
     python bench.py [--steps K] [--warmup W] [--config 3b] [--no-cpu-baseline]
+    python bench.py --config 3b_stack [--no-recompute]     (the whole 28-block model)
 
 A step is one ls_block_fwd_bwd call (RMSNorm, QKV + RoPE, causal GQA flash
 attention, output projection, RMSNorm, SwiGLU MLP, and the whole backward with
@@ -137,6 +138,72 @@ def kernel_only(args):
     print(json.dumps(out), flush=True)
 
 
+def stack_bench(args):
+    """--config 3b_stack: the whole model (28 blocks, tied embedding and LM
+    head, cross-entropy) forward + backward per step, inputs drawn on the GPU."""
+    import torch
+
+    from paper_2510_02483_amd import configs, flops, inputs, lib
+
+    sc = configs.STACK_PRESETS[args.config].with_(recompute=not args.no_recompute)
+    log(f"config {sc}")
+    st = lib.Stack(sc, inputs.make_stack_inputs(sc, device="cuda"))
+    for _ in range(args.warmup):
+        st.step(accumulate=True)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    per_step = sc.n_layers * (2 if sc.recompute else 1)
+    lib.ls_timing_begin(DOMINANT, args.steps * per_step)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for _ in range(args.steps):
+        st.step(accumulate=True)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    n_dom, dom_ms = lib.ls_timing_end()
+    ms = start.elapsed_time(stop) / args.steps
+    fl = flops.stack_fwd_bwd_flops(sc)
+    tflops = fl / (ms * 1e-3) / 1e12
+    dom_tflops = dominant_flops(sc.block) / (dom_ms * 1e-3) / 1e12 if n_dom else None
+    c = sc.block
+    result = {
+        "metric": "model fwd+bwd TFLOP/s and MFU (bf16), 3B-shaped 28-block stack, 1 MI355X",
+        "value": round(tflops, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"3B-shaped {sc.n_layers}-block stack fwd+bwd with tied embedding, LM head and "
+                               f"cross-entropy, micro-batch {c.batch} x seq {c.seq}, vocab {sc.vocab}, "
+                               f"{'per-block recompute' if sc.recompute else 'no recompute (all saved states kept)'}",
+                   "n_layers": sc.n_layers, "vocab": sc.vocab, "batch": c.batch, "seq": c.seq,
+                   "hidden": c.hidden, "recompute": sc.recompute, "parallelism": "single GPU"},
+        "mfu": round(tflops / PEAK_BF16_TFLOPS, 4),
+        "tokens_per_s": round(sc.tokens / (ms * 1e-3), 1),
+        "model_flops_per_step": fl,
+        "loss": round(st.loss.item(), 4),
+        "roofline": {
+            "kernel": f"{DOMINANT} (bf16 MFMA GEMM [T,H]x[H,2I] + fused SwiGLU)",
+            "bound": "mfma",
+            "achieved": round(dom_tflops, 2) if dom_tflops else None,
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(dom_tflops / PEAK_BF16_TFLOPS, 4) if dom_tflops else None,
+            "traffic": None,
+            "launches": n_dom,
+            "mean_ms": round(dom_ms, 4),
+        },
+    }
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -150,6 +217,8 @@ def main():
     ap.add_argument("--kernel", choices=("gemm_nt", "attention"),
                     help="time one kernel family instead of the block step (for per-kernel counters)")
     ap.add_argument("--shape", default="8192,16384,3072", help="M,N,K of --kernel gemm_nt")
+    ap.add_argument("--no-recompute", action="store_true",
+                    help="stack configurations: keep every block's saved state instead of recomputing it")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -162,6 +231,11 @@ def main():
         return
     if args.kernel:
         kernel_only(args)
+        return
+    from paper_2510_02483_amd import configs as _configs
+
+    if args.config in _configs.STACK_PRESETS:
+        stack_bench(args)
         return
 
     import torch
