@@ -205,6 +205,37 @@ int ls_stack_fwd_bwd(const ls_stack_cfg* cfg, const int32_t* ids, const int32_t*
                      const ls_stack_grads* g, int accumulate, void* workspace,
                      size_t workspace_bytes, void* stream);
 
+/* ---- optimizer step ------------------------------------------------------------
+ *
+ * The report trains with AdamW (beta1 0.9, beta2 0.95, weight decay 0.01) and
+ * gradient clipping at global norm 1.0 (Section 2.4, Table 2).  One step over
+ * n parameters held in flat fp32 arrays (callers lay every tensor out in one
+ * arena; the first n_decay parameters take weight decay, the rest -- RMSNorm
+ * gains -- do not):
+ *
+ *   norm = ||grad||_2 over all n;  c = min(1, max_norm / (norm + 1e-6))
+ *   m = beta1 m + (1 - beta1) c grad;  v = beta2 v + (1 - beta2) (c grad)^2
+ *   master = master (1 - lr wd [i < n_decay]) - (lr / (1 - beta1^step)) m / (sqrt(v / (1 - beta2^step)) + eps)
+ *   param  = bf16(master)  (round to nearest even; skipped when param is NULL)
+ *
+ * grad is read only; grad_norm (NULL allowed) receives the norm before
+ * clipping.  The norm is summed in fp64 in a fixed order (deterministic).
+ * Every array: device memory, 16-byte aligned, no overlaps. */
+typedef struct {
+  float lr;
+  float beta1, beta2;  /* in [0, 1) */
+  float eps;           /* > 0 */
+  float weight_decay;  /* >= 0, lr * weight_decay < 1 */
+  float max_norm;      /* <= 0: no clipping */
+  int32_t step;        /* 1-based step count t */
+} ls_adamw_cfg;
+
+/* Workspace bytes of ls_adamw_step (independent of n). */
+size_t ls_adamw_workspace(void);
+int ls_adamw_step(int64_t n, int64_t n_decay, const ls_adamw_cfg* cfg, float* master,
+                  ls_bf16* param, const float* grad, float* m, float* v, float* grad_norm,
+                  void* workspace, size_t workspace_bytes, void* stream);
+
 /* ---- single-kernel entry points (used for per-kernel parity) ---------------- */
 
 /* Causal attention core on a packed projection buffer.
@@ -287,7 +318,8 @@ int ls_gemm_tile_override(int32_t bm, int32_t bn);
  * "output projection", "gate/up projection", "down projection", "dact",
  * "dWd", "dh2", "dWg/dWu", "rmsnorm bwd", "dO", "dWo", "attention bwd",
  * "dh1", "dWqkv", and in ls_stack_fwd_bwd also "embedding fwd", "targets",
- * "logits", "cross-entropy", "dh head", "dE head", "loss", "embedding bwd"),
+ * "logits", "cross-entropy", "dh head", "dE head", "loss", "embedding bwd",
+ * and "adamw" for ls_adamw_step),
  * creating up to max_launches event pairs up front;
  * later calls record into them without allocating.  ls_timing_end waits for
  * the recorded events, writes the number of recorded launches and their mean

@@ -1135,4 +1135,33 @@ int ls_embed_bwd(int64_t tokens, int32_t hidden, int32_t vocab, const int32_t* i
   return LS_OK;
 }
 
+
+size_t ls_adamw_workspace(void) { return ls::adamw_workspace(); }
+
+int ls_adamw_step(int64_t n, int64_t n_decay, const ls_adamw_cfg* cfg, float* master, ls_bf16* param,
+                  const float* grad, float* m, float* v, float* grad_norm, void* workspace, size_t workspace_bytes,
+                  void* stream) {
+  if (!cfg) return fail(LS_ERR_NULL, "cfg is NULL");
+  if (n <= 0 || n_decay < 0 || n_decay > n)
+    return fail(LS_ERR_SHAPE, "need n > 0 and 0 <= n_decay <= n (n = %lld, n_decay = %lld)", (long long)n,
+                (long long)n_decay);
+  if (cfg->step < 1) return fail(LS_ERR_SHAPE, "step must be >= 1 (got %d)", cfg->step);
+  if (!(cfg->beta1 >= 0.f && cfg->beta1 < 1.f) || !(cfg->beta2 >= 0.f && cfg->beta2 < 1.f) || !(cfg->eps > 0.f) ||
+      !(cfg->lr >= 0.f) || !(cfg->weight_decay >= 0.f) || !(cfg->lr * cfg->weight_decay < 1.f) ||
+      !(cfg->max_norm == cfg->max_norm))
+    return fail(LS_ERR_SHAPE, "hyper-parameters out of range (0 <= beta < 1, eps > 0, lr >= 0, 0 <= lr*wd < 1)");
+  const size_t f4 = (size_t)n * 4;
+  std::vector<Range> in{{grad, f4, "grad"}};
+  std::vector<Range> out{{master, f4, "master"}, {m, f4, "m"}, {v, f4, "v"}, {workspace, workspace_bytes, "workspace"}};
+  if (param) out.push_back({param, (size_t)n * 2, "param"});
+  if (grad_norm) out.push_back({grad_norm, 4, "grad_norm"});
+  if (int e = check_ranges(in, out)) return e;
+  if (workspace_bytes < ls::adamw_workspace())
+    return fail(LS_ERR_WORKSPACE, "workspace %zu < %zu bytes", workspace_bytes, ls::adamw_workspace());
+  ls::AdamwHyper h{cfg->lr, cfg->beta1, cfg->beta2, cfg->eps, cfg->weight_decay, cfg->max_norm, cfg->step};
+  const hipStream_t st = (hipStream_t)stream;
+  LS_STEP("adamw", st, ls::adamw_step(n, n_decay, h, master, (bf16_t*)param, grad, m, v, grad_norm, workspace, st));
+  return LS_OK;
+}
+
 }  // extern "C"

@@ -97,4 +97,16 @@ hipError_t ce_rows(int64_t rows, int V, bf16_t* z, const int32_t* tg, const int*
 // loss = sum(row_loss[0 .. T)) / max(counts[0], 1).
 hipError_t ce_loss(int64_t T, const float* row_loss, const int* counts, float* loss, hipStream_t s);
 
+// ---- optimizer ------------------------------------------------------------------
+struct AdamwHyper {
+  float lr, beta1, beta2, eps, weight_decay, max_norm;  // max_norm <= 0: no clipping
+  int step;                                            // t >= 1
+};
+// Workspace bytes of adamw_step (independent of n).
+size_t adamw_workspace();
+// Global-norm clip + AdamW over n fp32 parameters (decay on the first n_decay);
+// param (bf16 copy) and grad_norm may be null.
+hipError_t adamw_step(int64_t n, int64_t n_decay, const AdamwHyper& hp, float* master, bf16_t* param,
+                      const float* grad, float* m, float* v, float* grad_norm, void* ws, hipStream_t s);
+
 }  // namespace ls

@@ -62,6 +62,11 @@ class LsStackGrads(ctypes.Structure):
                 ("layers", ctypes.POINTER(LsBlockGrads))]
 
 
+class LsAdamwCfg(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float), ("eps", ctypes.c_float),
+                ("weight_decay", ctypes.c_float), ("max_norm", ctypes.c_float), ("step", ctypes.c_int32)]
+
+
 _lib = None
 _P = ctypes.c_void_p
 _PROTOS = {
@@ -92,6 +97,9 @@ _PROTOS = {
                                         ctypes.c_size_t, _P]),
     "ls_embed_fwd": (ctypes.c_int, [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _P, _P, _P, _P]),
     "ls_embed_bwd": (ctypes.c_int, [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _P, _P, _P, _P]),
+    "ls_adamw_workspace": (ctypes.c_size_t, []),
+    "ls_adamw_step": (ctypes.c_int, [ctypes.c_int64, ctypes.c_int64, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t,
+                                     _P]),
     "ls_timing_begin": (ctypes.c_int, [ctypes.c_char_p, ctypes.c_int]),
     "ls_timing_end": (ctypes.c_int, [_P, _P]),
 }
@@ -287,6 +295,23 @@ def ls_embed_bwd(ids, dx, d_embed, stream=None):
     _check(lib().ls_embed_bwd(ids.numel(), H, V, _p(ids), _p(dx), _p(d_embed), _stream(stream)), "ls_embed_bwd")
 
 
+def ls_adamw_workspace() -> int:
+    return lib().ls_adamw_workspace()
+
+
+def ls_adamw_step(master, param, grad, m, v, *, step, lr, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.01,
+                  max_norm=1.0, n_decay=None, grad_norm=None, workspace=None, stream=None):
+    """One clipped AdamW step over flat fp32 tensors (param: bf16 copy or None)."""
+    n = master.numel()
+    nd = n if n_decay is None else int(n_decay)
+    cfg = LsAdamwCfg(lr, beta1, beta2, eps, weight_decay, 0.0 if max_norm is None else max_norm, int(step))
+    if workspace is None:
+        workspace = torch.empty(ls_adamw_workspace(), dtype=torch.uint8, device=master.device)
+    _check(lib().ls_adamw_step(n, nd, ctypes.byref(cfg), _p(master), _p(param), _p(grad), _p(m), _p(v),
+                               _p(grad_norm), _p(workspace), workspace.numel() * workspace.element_size(),
+                               _stream(stream)), "ls_adamw_step")
+
+
 def ls_timing_begin(label: str, max_launches: int):
     _check(lib().ls_timing_begin(label.encode(), int(max_launches)), "ls_timing_begin")
 
@@ -324,29 +349,76 @@ class Block:
                          self.workspace, stream)
 
 
+DECAYED = ("wq", "wk", "wv", "wo", "wg", "wu", "wd")
+NOT_DECAYED = ("attn_norm", "mlp_norm")
+
+
 class Stack:
-    """Device buffers for one stack configuration plus a call of ls_stack_fwd_bwd.
+    """Device buffers for one stack configuration plus a call of ls_stack_fwd_bwd
+    and an optimizer step.
 
     ``host`` is the dict of inputs.make_stack_inputs (CPU or device tensors);
-    everything is moved to the device once.  Gradients are fp32."""
+    everything is moved to the device once.  All bf16 weights are views into
+    one arena and all fp32 gradients into another, in the same order: the
+    tensors that take weight decay first (embedding, then each block's seven
+    projections), then the RMSNorm gains (final, then each block's two), so
+    that one ls_adamw_step call updates the whole model."""
 
     def __init__(self, sc: StackConfig, host: dict, device="cuda", targets=None):
         self.cfg = sc
         dev = torch.device(device)
         self.ids = host["ids"].to(dev).reshape(-1).contiguous()
         self.targets = None if targets is None else targets.to(dev).reshape(-1).contiguous()
-        self.embed = host["embed"].to(dev).contiguous()
-        self.final_norm = host["final_norm"].to(dev).contiguous()
-        self.layers = [{n: l[n].to(dev).contiguous() for n in WEIGHTS} for l in host["layers"]]
-        self.d_embed = torch.zeros(self.embed.shape, dtype=torch.float32, device=dev)
-        self.d_final_norm = torch.zeros(self.final_norm.shape, dtype=torch.float32, device=dev)
-        self.d_layers = [{n: torch.zeros(w[n].shape, dtype=torch.float32, device=dev) for n in WEIGHTS}
-                         for w in self.layers]
+        order = [("embed", None)] + [(n, l) for l in range(sc.n_layers) for n in DECAYED]
+        order_nd = [("final_norm", None)] + [(n, l) for l in range(sc.n_layers) for n in NOT_DECAYED]
+
+        def src(name, l):
+            return host[name] if l is None else host["layers"][l][name]
+
+        sizes = [src(n, l).numel() for n, l in order + order_nd]
+        self.n_params = sum(sizes)
+        self.n_decay = sum(sizes[:len(order)])
+        self.w_arena = torch.empty(self.n_params, dtype=torch.bfloat16, device=dev)
+        self.g_arena = torch.zeros(self.n_params, dtype=torch.float32, device=dev)
+        self.layers = [dict() for _ in range(sc.n_layers)]
+        self.d_layers = [dict() for _ in range(sc.n_layers)]
+        off = 0
+        for (name, l), k in zip(order + order_nd, sizes):
+            t = src(name, l)
+            w = self.w_arena[off:off + k].view(t.shape)
+            w.copy_(t.to(dev))
+            g = self.g_arena[off:off + k].view(t.shape)
+            if l is None:
+                setattr(self, name, w)
+                setattr(self, "d_" + name, g)
+            else:
+                self.layers[l][name] = w
+                self.d_layers[l][name] = g
+            off += k
         self.loss = torch.zeros(1, dtype=torch.float32, device=dev)
         self.row_loss = torch.zeros(sc.tokens, dtype=torch.float32, device=dev)
         self.workspace = torch.empty(ls_stack_workspace(sc), dtype=torch.uint8, device=dev)
+        self.master = None
 
     def step(self, accumulate=False, stream=None):
         ls_stack_fwd_bwd(self.cfg, self.ids, self.targets, self.embed, self.final_norm, self.layers, self.loss,
                          self.row_loss, self.d_embed, self.d_final_norm, self.d_layers, accumulate, self.workspace,
                          stream)
+
+    def init_optimizer(self):
+        """fp32 master weights (from the bf16 weights) and zero moments."""
+        self.master = self.w_arena.float()
+        self.m = torch.zeros_like(self.master)
+        self.v = torch.zeros_like(self.master)
+        self.grad_norm = torch.zeros(1, dtype=torch.float32, device=self.master.device)
+        self.opt_workspace = torch.empty(ls_adamw_workspace(), dtype=torch.uint8, device=self.master.device)
+        self.opt_steps = 0
+
+    def optimizer_step(self, lr, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.01, max_norm=1.0, stream=None):
+        """Clipped AdamW over the whole model; rewrites the bf16 weights."""
+        if self.master is None:
+            self.init_optimizer()
+        self.opt_steps += 1
+        ls_adamw_step(self.master, self.w_arena, self.g_arena, self.m, self.v, step=self.opt_steps, lr=lr,
+                      beta1=beta1, beta2=beta2, eps=eps, weight_decay=weight_decay, max_norm=max_norm,
+                      n_decay=self.n_decay, grad_norm=self.grad_norm, workspace=self.opt_workspace, stream=stream)

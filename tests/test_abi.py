@@ -207,3 +207,28 @@ def test_cross_entropy_and_embedding_argument_checks():
     assert lib.ls_embed_fwd(10, 12, 100, V(ids), V(z), V(rows), None) == 2
     assert lib.ls_embed_fwd(10, 16, 100, V(ids), V(z), V(ids), None) == 5
     assert lib.ls_embed_bwd(10, 16, 100, None, V(z), V(rows), None) == 1
+
+
+def test_adamw_argument_checks():
+    lib = L.lib()
+    V = ctypes.c_void_p
+    ws_need = lib.ls_adamw_workspace()
+    assert ws_need >= 2048 * 8
+    cfg = L.LsAdamwCfg(1e-3, 0.9, 0.95, 1e-8, 0.01, 1.0, 1)
+    p, w, g, m, v, nrm, ws = (1 << 32), (1 << 33), (1 << 34), (1 << 35), (1 << 36), (1 << 37), (1 << 38)
+    call = lambda n, nd, c, p_=p, g_=g, n_ws=ws_need: lib.ls_adamw_step(  # noqa: E731
+        n, nd, ctypes.byref(c), V(p_), V(w), V(g_), V(m), V(v), V(nrm), V(ws), n_ws, None)
+    assert call(0, 0, cfg) == 2
+    assert call(100, 101, cfg) == 2
+    assert call(100, -1, cfg) == 2
+    assert call(100, 50, cfg, g_=p + 16) == 5        # grad overlaps master
+    assert call(100, 50, cfg, p_=p + 4) == 4         # misaligned
+    assert call(100, 50, cfg, n_ws=ws_need - 8) == 6
+    for field, value in [("step", 0), ("beta1", 1.0), ("beta2", -0.1), ("eps", 0.0), ("lr", -1.0),
+                         ("weight_decay", -0.01)]:
+        bad = L.LsAdamwCfg(1e-3, 0.9, 0.95, 1e-8, 0.01, 1.0, 1)
+        setattr(bad, field, value)
+        assert call(100, 50, bad) == 2, field
+    assert lib.ls_adamw_step(100, 50, None, V(p), V(w), V(g), V(m), V(v), None, V(ws), ws_need, None) == 1
+    assert lib.ls_adamw_step(100, 50, ctypes.byref(cfg), V(p), None, V(g), V(m), None, None, V(ws), ws_need,
+                             None) == 1
