@@ -138,6 +138,31 @@ def kernel_only(args):
     print(json.dumps(out), flush=True)
 
 
+ADAMW_BYTES_PER_PARAM = 34  # norm pass: read the fp32 gradient (4); update: read 16, write 14
+
+
+def energy_of(step_fn, tokens_per_step: int, args):
+    """GPU energy of repeated steps over about --energy-seconds (None figures
+    when the energy counter cannot be read)."""
+    import torch
+
+    from paper_2510_02483_amd import energy
+
+    if args.energy_seconds <= 0:
+        return None
+    meter = energy.EnergyMeter()
+
+    def one():
+        step_fn()
+        torch.cuda.synchronize()
+
+    calls, secs, joules = meter.measure(one, args.energy_seconds)
+    out = energy.report(calls, secs, joules, tokens_per_step)
+    if meter.error:
+        out["error"] = meter.error
+    return out
+
+
 def stack_bench(args):
     """--config 3b_stack: the whole model (28 blocks, tied embedding and LM
     head, cross-entropy) forward + backward per step, inputs drawn on the GPU."""
@@ -163,6 +188,17 @@ def stack_bench(args):
     torch.cuda.synchronize()
     n_dom, dom_ms = lib.ls_timing_end()
     ms = start.elapsed_time(stop) / args.steps
+    # the optimizer step (once per global batch in training): clipped AdamW over every parameter
+    st.init_optimizer()
+    st.optimizer_step(lr=1e-5)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for _ in range(args.steps):
+        st.optimizer_step(lr=1e-5)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    opt_ms = start.elapsed_time(stop) / args.steps
+    energy = energy_of(lambda: st.step(accumulate=True), sc.tokens, args)
     fl = flops.stack_fwd_bwd_flops(sc)
     tflops = fl / (ms * 1e-3) / 1e12
     dom_tflops = dominant_flops(sc.block) / (dom_ms * 1e-3) / 1e12 if n_dom else None
@@ -189,6 +225,13 @@ def stack_bench(args):
         "tokens_per_s": round(sc.tokens / (ms * 1e-3), 1),
         "model_flops_per_step": fl,
         "loss": round(st.loss.item(), 4),
+        "optimizer": {"kernel": "clipped AdamW over flat fp32 arrays (ls_adamw_step)", "bound": "hbm",
+                      "params": st.n_params, "ms": round(opt_ms, 3),
+                      "bytes_per_param": ADAMW_BYTES_PER_PARAM,
+                      "achieved_gbs": round(ADAMW_BYTES_PER_PARAM * st.n_params / (opt_ms * 1e-3) / 1e9, 1),
+                      "peak_gbs": PEAK_HBM_GBS,
+                      "frac": round(ADAMW_BYTES_PER_PARAM * st.n_params / (opt_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)},
+        "energy": energy,
         "roofline": {
             "kernel": f"{DOMINANT} (bf16 MFMA GEMM [T,H]x[H,2I] + fused SwiGLU)",
             "bound": "mfma",
@@ -217,6 +260,8 @@ def main():
     ap.add_argument("--kernel", choices=("gemm_nt", "attention"),
                     help="time one kernel family instead of the block step (for per-kernel counters)")
     ap.add_argument("--shape", default="8192,16384,3072", help="M,N,K of --kernel gemm_nt")
+    ap.add_argument("--energy-seconds", type=float, default=2.0,
+                    help="seconds of extra steps read against the GPU energy counter (0: skip)")
     ap.add_argument("--no-recompute", action="store_true",
                     help="stack configurations: keep every block's saved state instead of recomputing it")
     args = ap.parse_args()
@@ -264,6 +309,7 @@ def main():
     n_dom, dom_ms = lib.ls_timing_end()
     ms = start.elapsed_time(stop) / args.steps
 
+    energy = energy_of(lambda: blk.step(accumulate=True), c.tokens, args)
     fl = flops.block_fwd_bwd_flops(c)
     tflops = fl / (ms * 1e-3) / 1e12
     dom_tflops = dominant_flops(c) / (dom_ms * 1e-3) / 1e12 if n_dom else None
@@ -288,6 +334,7 @@ def main():
         "tokens_per_s": round(c.tokens / (ms * 1e-3), 1),
         "model_flops_per_step": fl,
         "tflops_noncausal_convention": round(flops.block_fwd_bwd_flops(c, causal=False) / (ms * 1e-3) / 1e12, 2),
+        "energy": energy,
         "roofline": {
             "kernel": f"{DOMINANT} (bf16 MFMA GEMM [T,H]x[H,2I] + fused SwiGLU)",
             "bound": "mfma",
