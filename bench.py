@@ -21,7 +21,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
-METRIC = "decoder-block fwd+bwd TFLOP/s and MFU (bf16), 3B shape seq 2048, 1 MI355X"
+METRIC = "decoder-block fwd+bwd TFLOP/s and MFU (bf16), 3B shape seq 2048, 1 MI355X"  # the default --config 3b
 PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 matrix peak (256 CUs x 4096 FLOP/clk x 2.4 GHz)
 PEAK_HBM_GBS = 8000.0
 DOMINANT = "gate/up projection"  # the largest single kernel launch of the step
@@ -138,6 +138,8 @@ def kernel_only(args):
     print(json.dumps(out), flush=True)
 
 
+WORKLOAD_NAMES = {"3b": "Llama-3.2-3B-shaped", "3b_8k": "Llama-3.2-3B-shaped", "30b": "Llama-30B-shaped (52 x 128 heads)",
+                  "paper_3b": "Table-1 3B-shaped (hidden 2048, 16q/2kv, SwiGLU 11008)", "tiny": "tiny"}
 ADAMW_BYTES_PER_PARAM = 34  # norm pass: read the fp32 gradient (4); update: read 16, write 14
 
 
@@ -204,7 +206,7 @@ def stack_bench(args):
     dom_tflops = dominant_flops(sc.block) / (dom_ms * 1e-3) / 1e12 if n_dom else None
     c = sc.block
     result = {
-        "metric": "model fwd+bwd TFLOP/s and MFU (bf16), 3B-shaped 28-block stack, 1 MI355X",
+        "metric": f"model fwd+bwd TFLOP/s and MFU (bf16), {sc.name} ({sc.n_layers} blocks), 1 MI355X",
         "value": round(tflops, 2),
         "unit": "TFLOP/s",
         "n_gpus": 1,
@@ -216,7 +218,7 @@ def stack_bench(args):
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": f"3B-shaped {sc.n_layers}-block stack fwd+bwd with tied embedding, LM head and "
+        "config": {"workload": f"{sc.name}: {sc.n_layers}-block stack fwd+bwd with tied embedding, LM head and "
                                f"cross-entropy, micro-batch {c.batch} x seq {c.seq}, vocab {sc.vocab}, "
                                f"{'per-block recompute' if sc.recompute else 'no recompute (all saved states kept)'}",
                    "n_layers": sc.n_layers, "vocab": sc.vocab, "batch": c.batch, "seq": c.seq,
@@ -224,6 +226,9 @@ def stack_bench(args):
         "mfu": round(tflops / PEAK_BF16_TFLOPS, 4),
         "tokens_per_s": round(sc.tokens / (ms * 1e-3), 1),
         "model_flops_per_step": fl,
+        "tflops_paper_convention": round(flops.training_flops_per_token(
+            sc.n_layers, c.hidden, c.n_q_heads, c.n_kv_heads, c.intermediate, sc.vocab, c.seq) * sc.tokens
+            / (ms * 1e-3) / 1e12, 2),
         "loss": round(st.loss.item(), 4),
         "optimizer": {"kernel": "clipped AdamW over flat fp32 arrays (ls_adamw_step)", "bound": "hbm",
                       "params": st.n_params, "ms": round(opt_ms, 3),
@@ -314,7 +319,7 @@ def main():
     tflops = fl / (ms * 1e-3) / 1e12
     dom_tflops = dominant_flops(c) / (dom_ms * 1e-3) / 1e12 if n_dom else None
     result = {
-        "metric": METRIC,
+        "metric": METRIC if args.config == "3b" else f"decoder-block fwd+bwd TFLOP/s and MFU (bf16), {c.name}, 1 MI355X",
         "value": round(tflops, 2),
         "unit": "TFLOP/s",
         "n_gpus": 1,
@@ -326,7 +331,7 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": f"Llama-3.2-3B-shaped decoder block fwd+bwd, batch {c.batch} x seq {c.seq}",
+        "config": {"workload": f"{WORKLOAD_NAMES.get(c.name, c.name)} decoder block fwd+bwd, batch {c.batch} x seq {c.seq}",
                    "batch": c.batch, "seq": c.seq, "hidden": c.hidden, "n_q_heads": c.n_q_heads,
                    "n_kv_heads": c.n_kv_heads, "head_dim": c.head_dim, "intermediate": c.intermediate,
                    "rope_theta": c.rope_theta, "parallelism": "single GPU"},

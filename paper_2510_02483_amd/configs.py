@@ -57,7 +57,12 @@ B3_8K = BlockConfig("3b_8k", 2, batch=1, seq=8192, hidden=3072, n_q_heads=24, n_
 B30 = BlockConfig("30b", 3, batch=2, seq=2048, hidden=6656, n_q_heads=52, n_kv_heads=52,
                   head_dim=128, intermediate=17920, rope_theta=1e4)
 
-PRESETS = {c.name: c for c in (TINY, B3, B3_8K, B30)}
+# The report's own 3B model (Table 1: hidden 2048, 16 query / 2 kv heads of 128,
+# SwiGLU 11008) at sequence 4096, micro-batch 2.
+PAPER_3B = BlockConfig("paper_3b", 8, batch=2, seq=4096, hidden=2048, n_q_heads=16, n_kv_heads=2,
+                       head_dim=128, intermediate=11008, rope_theta=1e4)
+
+PRESETS = {c.name: c for c in (TINY, B3, B3_8K, B30, PAPER_3B)}
 
 
 @dataclass(frozen=True)
@@ -84,4 +89,8 @@ TINY_STACK = StackConfig("tiny_stack", TINY.with_(name="tiny_stack_block", cfg_i
 # Llama-3.2-3B-shaped model: 28 blocks, vocabulary 128256, micro-batch 4 x 2048.
 STACK_3B = StackConfig("3b_stack", B3.with_(name="3b_stack_block", cfg_id=4), n_layers=28, vocab=128256)
 
-STACK_PRESETS = {c.name: c for c in (TINY_STACK, STACK_3B)}
+# The report's 3B model whole (Table 1: 28 blocks; vocabulary 32000), micro-batch 2 x 4096.
+PAPER_3B_STACK = StackConfig("paper_3b_stack", PAPER_3B.with_(name="paper_3b_stack_block", cfg_id=9),
+                             n_layers=28, vocab=32000)
+
+STACK_PRESETS = {c.name: c for c in (TINY_STACK, STACK_3B, PAPER_3B_STACK)}

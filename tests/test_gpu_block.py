@@ -203,3 +203,13 @@ def test_block_30b_full_size_prefix():
     blk2.step()
     torch.cuda.synchronize()
     assert np.array_equal(y_all[[1, 0]], f64(blk2.y).reshape(c.batch, c.seq, c.hidden))
+
+
+def test_block_paper_3b_full_size_prefix():
+    """The report's own 3B block (Table 1: hidden 2048, 16 query heads sharing
+    2 kv heads, SwiGLU 11008) at batch 2 x seq 4096, full launch
+    configuration; oracle on the first 768 tokens of sequence 1."""
+    need_gpu()
+    c = configs.PAPER_3B
+    say(f"paper 3b full size {c}")
+    _prefix_parity(c, 768, sample_seq=1)

@@ -210,3 +210,26 @@ def test_stack_3b_full_size_prefix():
         for n in L.WEIGHTS:
             assert torch.equal(st2.d_layers[l][n], g1[l][n]), (l, n)
     assert fro_rel(f64(st2.d_embed), f64(dE1)) < 1e-6
+
+
+def test_stack_paper_3b_full_size_prefix():
+    """The report's 3B model shapes (Table 1; vocabulary 32000, micro-batch
+    2 x 4096) at depth 2: targets on the first 384 tokens of sequence 0,
+    checked against the oracle on that prefix."""
+    need_gpu()
+    sc = configs.PAPER_3B_STACK.with_(n_layers=2)
+    t0, b = 384, 0
+    say(f"paper 3b stack full-size prefix {sc} t0={t0}")
+    host = inputs.make_stack_inputs(sc, e_std=0.1, gamma="random")
+    S = sc.block.seq
+    tg = torch.full((sc.block.batch, S), -1, dtype=torch.int32)
+    tg[b, :t0] = host["ids"][b, 1:t0 + 1]
+    tg = tg.reshape(-1)
+    st = L.Stack(sc, host, targets=tg)
+    st.step()
+    torch.cuda.synchronize()
+    ref = oracle_stack(sc, host, targets=tg, batch_rows=(b, t0))
+    sel = np.zeros(sc.tokens, dtype=bool)
+    sel[b * S:b * S + t0] = True
+    assert np.all(f64(st.row_loss)[~sel] == 0.0)
+    compare_stack(st, ref, rows_sel=sel)
