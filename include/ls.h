@@ -58,7 +58,7 @@ typedef enum {
   LS_OK = 0,
   LS_ERR_NULL = 1,        /* a required pointer is NULL */
   LS_ERR_SHAPE = 2,       /* a size is non-positive, inconsistent or not a multiple of 8 */
-  LS_ERR_UNSUPPORTED = 3, /* valid but not implemented (head_dim not 64 or 128) */
+  LS_ERR_UNSUPPORTED = 3, /* valid but not implemented (e.g. a head_dim below 64 or above 128) */
   LS_ERR_ALIGN = 4,       /* a pointer is not 16-byte aligned */
   LS_ERR_ALIAS = 5,       /* an output buffer overlaps an input or another output */
   LS_ERR_WORKSPACE = 6,   /* workspace or saved-state buffer too small */
@@ -66,8 +66,11 @@ typedef enum {
 } ls_status;
 
 /* Shape of one decoder block.  Requirements: all sizes > 0; n_q_heads is a
- * multiple of n_kv_heads; head_dim is 64 or 128; hidden and intermediate are
- * multiples of 8; rms_eps >= 0, rope_theta > 1. */
+ * multiple of n_kv_heads; head_dim is 64, or a multiple of 8 from 72 to 128
+ * (sizes other than 64 and 128, such as the 104 of a 64-head 6656-wide model,
+ * run in 128-wide slots: each head's two RoPE halves are placed at slot
+ * offsets 0 and 64 with zero features between, which changes no result);
+ * hidden and intermediate are multiples of 8; rms_eps >= 0, rope_theta > 1. */
 typedef struct {
   int32_t batch;
   int32_t seq;
@@ -242,7 +245,8 @@ int ls_adamw_step(int64_t n, int64_t n_decay, const ls_adamw_cfg* cfg, float* ma
  * qkv: [batch*seq, (n_q_heads + 2*n_kv_heads)*head_dim] bf16, row = token,
  * columns = q heads, then k heads, then v heads (q and k already rotated).
  * o: [batch*seq, n_q_heads*head_dim] bf16.  lse: [batch, n_q_heads, seq] fp32.
- * Only batch, seq, n_q_heads, n_kv_heads, head_dim of *cfg are used. */
+ * Only batch, seq, n_q_heads, n_kv_heads, head_dim of *cfg are used; head_dim
+ * must be 64 or 128 here (LS_ERR_UNSUPPORTED otherwise). */
 int ls_attn_core_fwd(const ls_block_cfg* cfg, const ls_bf16* qkv, ls_bf16* o, float* lse,
                      void* stream);
 

@@ -16,7 +16,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libls.so")
-SOURCES = ("abi.hip", "gemm.hip", "attention.hip", "norm.hip", "lmhead.hip", "optim.hip")
+SOURCES = ("abi.hip", "gemm.hip", "attention.hip", "norm.hip", "lmhead.hip", "optim.hip", "headpad.hip")
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -62,7 +62,12 @@ B30 = BlockConfig("30b", 3, batch=2, seq=2048, hidden=6656, n_q_heads=52, n_kv_h
 PAPER_3B = BlockConfig("paper_3b", 8, batch=2, seq=4096, hidden=2048, n_q_heads=16, n_kv_heads=2,
                        head_dim=128, intermediate=11008, rope_theta=1e4)
 
-PRESETS = {c.name: c for c in (TINY, B3, B3_8K, B30, PAPER_3B)}
+# The report's own 30B block (Table 1: hidden 6656, 64 heads of 104, multi-head,
+# SwiGLU 17920) at sequence 4096, micro-batch 2.
+PAPER_30B = BlockConfig("paper_30b", 12, batch=2, seq=4096, hidden=6656, n_q_heads=64, n_kv_heads=64,
+                        head_dim=104, intermediate=17920, rope_theta=1e4)
+
+PRESETS = {c.name: c for c in (TINY, B3, B3_8K, B30, PAPER_3B, PAPER_30B)}
 
 
 @dataclass(frozen=True)

@@ -76,8 +76,13 @@ void timing_mark(const char* label, hipStream_t st, bool start) {
     timing_mark(label, st, false);                      \
   } while (0)
 
+// Head sizes the attention kernels tile natively are 64 and 128; a size in
+// between is held in 128-wide slots (dp = 128, `pad`), and Pq, Pkv, Pqkv are
+// the widths of q, k/v and qkv in that layout (equal to Dq, Dkv, Dqkv otherwise).
 struct Dims {
   int64_t B, S, T, H, nq, nkv, d, Dq, Dkv, Dqkv, I;
+  int64_t dp, Pq, Pkv, Pqkv;
+  bool pad;
 };
 
 Dims dims_of(const ls_block_cfg& c) {
@@ -93,6 +98,11 @@ Dims dims_of(const ls_block_cfg& c) {
   m.Dkv = m.nkv * m.d;
   m.Dqkv = m.Dq + 2 * m.Dkv;
   m.I = c.intermediate;
+  m.dp = (m.d == 64 || m.d == 128) ? m.d : 128;
+  m.pad = m.dp != m.d;
+  m.Pq = m.nq * m.dp;
+  m.Pkv = m.nkv * m.dp;
+  m.Pqkv = m.Pq + 2 * m.Pkv;
   return m;
 }
 
@@ -107,16 +117,17 @@ int check_cfg(const ls_block_cfg* c) {
     return fail(LS_ERR_SHAPE, "hidden (%d) and intermediate (%d) must be multiples of 8", c->hidden, c->intermediate);
   if (!(c->rope_theta > 1.0f) || !(c->rms_eps >= 0.0f))
     return fail(LS_ERR_SHAPE, "rope_theta must exceed 1 and rms_eps must be >= 0");
-  if (c->head_dim != 64 && c->head_dim != 128)
-    return fail(LS_ERR_UNSUPPORTED, "head_dim %d is not supported (64 or 128)", c->head_dim);
+  if (c->head_dim != 64 && !(c->head_dim > 64 && c->head_dim <= 128 && c->head_dim % 8 == 0))
+    return fail(LS_ERR_UNSUPPORTED, "head_dim %d is not supported (64, or a multiple of 8 from 72 to 128)",
+                c->head_dim);
   if (c->hidden > 8192) return fail(LS_ERR_UNSUPPORTED, "hidden %d exceeds 8192", c->hidden);
   const Dims m = dims_of(*c);
   const int64_t lim = (int64_t)1 << 30;
   // every matrix is addressed with 32-bit byte offsets (buffer loads, whose
   // resources stay below 2047 MiB)
-  const int64_t widest = std::max(std::max(m.Dqkv, 2 * m.I), m.H);
-  if (m.T >= lim || m.Dqkv >= lim || 2 * m.I >= lim || m.T * widest * 2 >= kMaxBytes ||
-      m.I * m.H * 2 >= kMaxBytes || m.Dqkv * m.H * 2 >= kMaxBytes)
+  const int64_t widest = std::max(std::max(m.Pqkv, 2 * m.I), m.H);
+  if (m.T >= lim || m.Pqkv >= lim || 2 * m.I >= lim || m.T * widest * 2 >= kMaxBytes ||
+      m.I * m.H * 2 >= kMaxBytes || m.Pqkv * m.H * 4 >= kMaxBytes)
     return fail(LS_ERR_SHAPE, "problem too large (a matrix reaches 2047 MiB)");
   return LS_OK;
 }
@@ -172,8 +183,8 @@ AttnSaved attn_saved_layout(const Dims& m) {
   Carver c;
   AttnSaved s;
   s.h1 = c.take(m.T * m.H * 2);
-  s.qkv = c.take(m.T * m.Dqkv * 2);
-  s.o = c.take(m.T * m.Dq * 2);
+  s.qkv = c.take(m.T * m.Pqkv * 2);
+  s.o = c.take(m.T * m.Pq * 2);
   s.r1 = c.take(m.T * 4);
   s.lse = c.take(m.B * m.nq * m.S * 4);
   s.total = c.off;
@@ -197,18 +208,23 @@ MlpSaved mlp_saved_layout(const Dims& m) {
 size_t norm_partial_bytes(const Dims& m) { return (size_t)ls::rmsnorm_bwd_parts(m.T) * m.H * 4; }
 
 ls::AttnShape attn_shape(const Dims& m) {
-  return ls::AttnShape{(int)m.B, (int)m.S, (int)m.nq, (int)m.nkv, (int)m.d};
+  return ls::AttnShape{(int)m.B, (int)m.S, (int)m.nq, (int)m.nkv, (int)m.dp, (int)m.d};
 }
 
 struct AttnWs {
-  size_t rope, dO, dqkv, dh1, partial, core, total;
+  size_t rope, dO, dqkv, dh1, partial, core, wpad, wopad, gpad, gopad, total;
 };
 AttnWs attn_ws_layout(const Dims& m) {
   Carver c;
   AttnWs w;
-  w.rope = c.take(m.S * m.d * 4);  // cos and sin, S x d/2 each
-  w.dO = c.take(m.T * m.Dq * 2);
-  w.dqkv = c.take(m.T * m.Dqkv * 2);
+  w.rope = c.take(m.S * m.dp * 4);  // cos and sin, S x dp/2 each
+  w.dO = c.take(m.T * m.Pq * 2);
+  w.dqkv = c.take(m.T * m.Pqkv * 2);
+  // padded layout only: Wq|Wk|Wv [Pqkv, H] and Wo [H, Pq] in bf16, their fp32 gradients
+  w.wpad = c.take(m.pad ? m.Pqkv * m.H * 2 : 0);
+  w.wopad = c.take(m.pad ? m.H * m.Pq * 2 : 0);
+  w.gpad = c.take(m.pad ? m.Pqkv * m.H * 4 : 0);
+  w.gopad = c.take(m.pad ? m.H * m.Pq * 4 : 0);
   w.dh1 = c.take(m.T * m.H * 2);
   w.partial = c.take(norm_partial_bytes(m));
   w.core = c.take(ls::attn_bwd_workspace(attn_shape(m)));
@@ -289,6 +305,26 @@ void grad_ranges(const Dims& m, const ls_block_grads* g, bool attn, bool mlp, st
 
 // ---- the sub-layers (arguments already checked) ------------------------------------
 
+// The projection weights in the layout the attention kernels read: the
+// caller's buffers, or (padded head layout) copies in the workspace.
+struct PaddedWeights {
+  const bf16_t *wq, *wk, *wv, *wo;
+  int err;
+};
+PaddedWeights padded_weights(const Dims& m, const ls_block_weights* w, void* ws, hipStream_t st) {
+  if (!m.pad) return {(const bf16_t*)w->wq, (const bf16_t*)w->wk, (const bf16_t*)w->wv, (const bf16_t*)w->wo, LS_OK};
+  const AttnWs wl = attn_ws_layout(m);
+  bf16_t* wp = at<bf16_t>(ws, wl.wpad);
+  bf16_t* wo = at<bf16_t>(ws, wl.wopad);
+  const int d = (int)m.d, dp = (int)m.dp, H = (int)m.H;
+  hipError_t e = ls::pad_head_rows((const bf16_t*)w->wq, wp, (int)m.nq, d, dp, H, st);
+  if (e == hipSuccess) e = ls::pad_head_rows((const bf16_t*)w->wk, wp + m.Pq * m.H, (int)m.nkv, d, dp, H, st);
+  if (e == hipSuccess) e = ls::pad_head_rows((const bf16_t*)w->wv, wp + (m.Pq + m.Pkv) * m.H, (int)m.nkv, d, dp, H, st);
+  if (e == hipSuccess) e = ls::pad_head_cols((const bf16_t*)w->wo, wo, H, (int)m.nq, d, dp, st);
+  if (e != hipSuccess) return {nullptr, nullptr, nullptr, nullptr, hip_fail(e, "padded weights")};
+  return {wp, wp + m.Pq * m.H, wp + (m.Pq + m.Pkv) * m.H, wo, LS_OK};
+}
+
 int run_attn_fwd(const ls_block_cfg& cfg, const Dims& m, const bf16_t* x, const ls_block_weights* w, bf16_t* x2,
                  void* saved, void* ws, hipStream_t st) {
   const AttnSaved sv = attn_saved_layout(m);
@@ -299,37 +335,39 @@ int run_attn_fwd(const ls_block_cfg& cfg, const Dims& m, const bf16_t* x, const 
   float* r1 = at<float>(saved, sv.r1);
   float* lse = at<float>(saved, sv.lse);
   float* cs = at<float>(ws, wl.rope);
+  const PaddedWeights pw = padded_weights(m, w, ws, st);
+  if (pw.err) return pw.err;
   LS_STEP("rmsnorm fwd", st, ls::rmsnorm_fwd(m.T, (int)m.H, cfg.rms_eps, x, (const bf16_t*)w->attn_norm, h1, r1, st));
-  LS_STEP("rope table", st, ls::rope_table((int)m.S, (int)m.d, (double)cfg.rope_theta, cs, st));
+  LS_STEP("rope table", st, ls::rope_table((int)m.S, (int)m.d, (double)cfg.rope_theta, cs, st, (int)m.dp));
   ls::GemmArgs g;
   g.M = (int)m.T;
-  g.N = (int)m.Dqkv;
+  g.N = (int)m.Pqkv;
   g.K = (int)m.H;
   g.A = h1;
   g.lda = m.H;
-  g.B[0] = (const bf16_t*)w->wq;
-  g.B[1] = (const bf16_t*)w->wk;
-  g.B[2] = (const bf16_t*)w->wv;
-  g.b_start[1] = (int)m.Dq;
-  g.b_start[2] = (int)(m.Dq + m.Dkv);
+  g.B[0] = pw.wq;
+  g.B[1] = pw.wk;
+  g.B[2] = pw.wv;
+  g.b_start[1] = (int)m.Pq;
+  g.b_start[2] = (int)(m.Pq + m.Pkv);
   g.ldb = m.H;
   g.epi = ls::EPI_ROPE;
   g.C = qkv;
-  g.ldc = m.Dqkv;
+  g.ldc = m.Pqkv;
   g.rope_cs = cs;
   g.seq = (int)m.S;
-  g.head_dim = (int)m.d;
-  g.rope_cols = (int)(m.Dq + m.Dkv);
+  g.head_dim = (int)m.dp;
+  g.rope_cols = (int)(m.Pq + m.Pkv);
   LS_STEP("qkv projection", st, ls::gemm(g, st));
   LS_STEP("attention fwd", st, ls::attn_fwd(attn_shape(m), qkv, o, lse, st));
   ls::GemmArgs p;
   p.M = (int)m.T;
   p.N = (int)m.H;
-  p.K = (int)m.Dq;
+  p.K = (int)m.Pq;
   p.A = o;
-  p.lda = m.Dq;
-  p.B[0] = (const bf16_t*)w->wo;
-  p.ldb = m.Dq;
+  p.lda = m.Pq;
+  p.B[0] = pw.wo;
+  p.ldb = m.Pq;
   p.epi = ls::EPI_RESID;
   p.R = x;
   p.C = x2;
@@ -354,52 +392,57 @@ int run_attn_bwd(const ls_block_cfg& cfg, const Dims& m, const bf16_t* x, const 
   bf16_t* dh1 = at<bf16_t>(ws, wl.dh1);
   float* partial = at<float>(ws, wl.partial);
   void* core = at<char>(ws, wl.core);
-  LS_STEP("rope table", st, ls::rope_table((int)m.S, (int)m.d, (double)cfg.rope_theta, cs, st));
+  const PaddedWeights pw = padded_weights(m, w, ws, st);
+  if (pw.err) return pw.err;
+  LS_STEP("rope table", st, ls::rope_table((int)m.S, (int)m.d, (double)cfg.rope_theta, cs, st, (int)m.dp));
   {  // dO = dx2 Wo
     ls::GemmArgs g;
     g.M = (int)m.T;
-    g.N = (int)m.Dq;
+    g.N = (int)m.Pq;
     g.K = (int)m.H;
     g.A = dx2;
     g.lda = m.H;
-    g.B[0] = (const bf16_t*)w->wo;
-    g.ldb = m.Dq;
+    g.B[0] = pw.wo;
+    g.ldb = m.Pq;
     g.b_kcontig = false;
     g.epi = ls::EPI_BF16;
     g.C = dO;
-    g.ldc = m.Dq;
+    g.ldc = m.Pq;
     LS_STEP("dO", st, ls::gemm(g, st));
   }
-  {  // dWo (+)= dx2^T o
+  {  // dWo (+)= dx2^T o  (padded layout: into the workspace, then folded back)
     ls::GemmArgs g;
     g.M = (int)m.H;
-    g.N = (int)m.Dq;
+    g.N = (int)m.Pq;
     g.K = (int)m.T;
     g.A = dx2;
     g.lda = m.H;
     g.a_kcontig = false;
     g.B[0] = o;
-    g.ldb = m.Dq;
+    g.ldb = m.Pq;
     g.b_kcontig = false;
     g.epi = ls::EPI_F32;
-    g.F[0] = gr->wo;
-    g.ldf = m.Dq;
-    g.accumulate = accumulate;
+    g.F[0] = m.pad ? at<float>(ws, wl.gopad) : gr->wo;
+    g.ldf = m.Pq;
+    g.accumulate = m.pad ? 0 : accumulate;
     LS_STEP("dWo", st, ls::gemm(g, st));
+    if (m.pad)
+      LS_STEP("dWo", st, ls::unpad_head_cols(at<float>(ws, wl.gopad), gr->wo, (int)m.H, (int)m.nq, (int)m.d,
+                                             (int)m.dp, accumulate, st));
   }
   LS_STEP("attention bwd", st, ls::attn_bwd(attn_shape(m), qkv, o, lse, dO, dqkv, cs, core, st));
   {  // dh1 = dq Wq + dk Wk + dv Wv
     ls::GemmArgs g;
     g.M = (int)m.T;
     g.N = (int)m.H;
-    g.K = (int)m.Dqkv;
+    g.K = (int)m.Pqkv;
     g.A = dqkv;
-    g.lda = m.Dqkv;
-    g.B[0] = (const bf16_t*)w->wq;
-    g.B[1] = (const bf16_t*)w->wk;
-    g.B[2] = (const bf16_t*)w->wv;
-    g.b_start[1] = (int)m.Dq;
-    g.b_start[2] = (int)(m.Dq + m.Dkv);
+    g.lda = m.Pqkv;
+    g.B[0] = pw.wq;
+    g.B[1] = pw.wk;
+    g.B[2] = pw.wv;
+    g.b_start[1] = (int)m.Pq;
+    g.b_start[2] = (int)(m.Pq + m.Pkv);
     g.ldb = m.H;
     g.b_kcontig = false;
     g.epi = ls::EPI_BF16;
@@ -407,26 +450,39 @@ int run_attn_bwd(const ls_block_cfg& cfg, const Dims& m, const bf16_t* x, const 
     g.ldc = m.H;
     LS_STEP("dh1", st, ls::gemm(g, st));
   }
-  {  // dWq, dWk, dWv (+)= dqkv^T h1
+  {  // dWq, dWk, dWv (+)= dqkv^T h1  (padded layout: into the workspace, then folded back)
     ls::GemmArgs g;
-    g.M = (int)m.Dqkv;
+    g.M = (int)m.Pqkv;
     g.N = (int)m.H;
     g.K = (int)m.T;
     g.A = dqkv;
-    g.lda = m.Dqkv;
+    g.lda = m.Pqkv;
     g.a_kcontig = false;
     g.B[0] = h1;
     g.ldb = m.H;
     g.b_kcontig = false;
     g.epi = ls::EPI_F32;
-    g.F[0] = gr->wq;
-    g.F[1] = gr->wk;
-    g.F[2] = gr->wv;
-    g.f_start[1] = (int)m.Dq;
-    g.f_start[2] = (int)(m.Dq + m.Dkv);
+    if (m.pad) {
+      g.F[0] = at<float>(ws, wl.gpad);
+      g.accumulate = 0;
+    } else {
+      g.F[0] = gr->wq;
+      g.F[1] = gr->wk;
+      g.F[2] = gr->wv;
+      g.f_start[1] = (int)m.Dq;
+      g.f_start[2] = (int)(m.Dq + m.Dkv);
+      g.accumulate = accumulate;
+    }
     g.ldf = m.H;
-    g.accumulate = accumulate;
     LS_STEP("dWqkv", st, ls::gemm(g, st));
+    if (m.pad) {
+      const float* gp = at<float>(ws, wl.gpad);
+      LS_STEP("dWqkv", st, ls::unpad_head_rows(gp, gr->wq, (int)m.nq, (int)m.d, (int)m.dp, (int)m.H, accumulate, st));
+      LS_STEP("dWqkv", st, ls::unpad_head_rows(gp + m.Pq * m.H, gr->wk, (int)m.nkv, (int)m.d, (int)m.dp, (int)m.H,
+                                               accumulate, st));
+      LS_STEP("dWqkv", st, ls::unpad_head_rows(gp + (m.Pq + m.Pkv) * m.H, gr->wv, (int)m.nkv, (int)m.d, (int)m.dp,
+                                               (int)m.H, accumulate, st));
+    }
   }
   LS_STEP("rmsnorm bwd", st,
           ls::rmsnorm_bwd(m.T, (int)m.H, x, (const bf16_t*)w->attn_norm, r1, dh1, dx2, dx, gr->attn_norm, accumulate,
@@ -798,8 +854,15 @@ int ls_timing_end(int* launches, float* mean_ms) {
 
 // ---- single-kernel entry points ------------------------------------------------------
 
-int ls_attn_core_fwd(const ls_block_cfg* cfg, const ls_bf16* qkv, ls_bf16* o, float* lse, void* stream) {
+static int check_core_cfg(const ls_block_cfg* cfg) {
   if (int e = check_cfg(cfg)) return e;
+  if (cfg->head_dim != 64 && cfg->head_dim != 128)
+    return fail(LS_ERR_UNSUPPORTED, "the attention core takes head_dim 64 or 128 (got %d)", cfg->head_dim);
+  return LS_OK;
+}
+
+int ls_attn_core_fwd(const ls_block_cfg* cfg, const ls_bf16* qkv, ls_bf16* o, float* lse, void* stream) {
+  if (int e = check_core_cfg(cfg)) return e;
   const Dims m = dims_of(*cfg);
   std::vector<Range> in{{qkv, (size_t)(m.T * m.Dqkv * 2), "qkv"}};
   std::vector<Range> out{{o, (size_t)(m.T * m.Dq * 2), "o"}, {lse, (size_t)(m.B * m.nq * m.S * 4), "lse"}};
@@ -809,13 +872,13 @@ int ls_attn_core_fwd(const ls_block_cfg* cfg, const ls_bf16* qkv, ls_bf16* o, fl
 }
 
 size_t ls_attn_core_bwd_workspace(const ls_block_cfg* cfg) {
-  if (check_cfg(cfg)) return 0;
+  if (check_core_cfg(cfg)) return 0;
   return ls::attn_bwd_workspace(attn_shape(dims_of(*cfg)));
 }
 
 int ls_attn_core_bwd(const ls_block_cfg* cfg, const ls_bf16* qkv, const ls_bf16* o, const float* lse,
                      const ls_bf16* dout, ls_bf16* dqkv, void* workspace, size_t workspace_bytes, void* stream) {
-  if (int e = check_cfg(cfg)) return e;
+  if (int e = check_core_cfg(cfg)) return e;
   const Dims m = dims_of(*cfg);
   const size_t need = ls::attn_bwd_workspace(attn_shape(m));
   std::vector<Range> in{{qkv, (size_t)(m.T * m.Dqkv * 2), "qkv"},

@@ -641,7 +641,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(AttnShape sh, const
 template <int D>
 hipError_t attn_fwd_t(const AttnShape& sh, const bf16_t* qkv, bf16_t* o, float* lse, hipStream_t s) {
   const unsigned grid = (unsigned)((sh.seq + BQ - 1) / BQ) * sh.nq * sh.batch;
-  const float sl2 = LOG2E / sqrtf((float)D);
+  const float sl2 = LOG2E / sqrtf((float)(sh.d_scale > 0 ? sh.d_scale : D));
   hipLaunchKernelGGL((attn_fwd_kernel<D>), dim3(grid), dim3(256), 0, s, sh, qkv, o, lse, sl2);
   return hipGetLastError();
 }
@@ -656,7 +656,7 @@ hipError_t attn_bwd_t(const AttnShape& sh, const bf16_t* qkv, const bf16_t* o, c
                      lse2);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const float scale = 1.0f / sqrtf((float)D);
+  const float scale = 1.0f / sqrtf((float)(sh.d_scale > 0 ? sh.d_scale : D));
   const unsigned gkv = (unsigned)((sh.seq + BWD_BKV - 1) / BWD_BKV) * sh.nkv * sh.batch;
   hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D>), dim3(gkv), dim3(256), 0, s, sh, qkv, dout, (const float*)lse2,
                      (const float*)Dv,

@@ -68,12 +68,15 @@ hipError_t rmsnorm_bwd(int64_t rows, int hidden, const bf16_t* x, const bf16_t* 
                        float* partial, hipStream_t s);
 
 // ---- RoPE table -------------------------------------------------------------
-// cs[p][i] = cos(p theta^(-2i/d)), cs[seq*d/2 + p*d/2 + i] = sin(...), computed in fp64.
-hipError_t rope_table(int seq, int head_dim, double theta, float* cs, hipStream_t s);
+// cs[p][i] = cos(p theta^(-2i/d)), cs[seq*t/2 + p*t/2 + i] = sin(...), computed in
+// fp64, for a table of t/2 entries per position (t = table_dim, 0 = head_dim);
+// entries i >= head_dim/2 of a wider table are cos 1, sin 0.
+hipError_t rope_table(int seq, int head_dim, double theta, float* cs, hipStream_t s, int table_dim = 0);
 
 // ---- attention ----------------------------------------------------------------
 struct AttnShape {
   int batch, seq, nq, nkv, d;
+  int d_scale = 0;  // features per head behind the softmax scale 1/sqrt(d_scale) (0: d)
 };
 hipError_t attn_fwd(const AttnShape& sh, const bf16_t* qkv, bf16_t* o, float* lse, hipStream_t s);
 // Workspace for attn_bwd: D and the base-2 log-sum-exp, [batch*nq*seq] fp32 each.
@@ -81,6 +84,15 @@ size_t attn_bwd_workspace(const AttnShape& sh);
 // rope_cs may be null (no inverse rotation of dq and dk).
 hipError_t attn_bwd(const AttnShape& sh, const bf16_t* qkv, const bf16_t* o, const float* lse,
                     const bf16_t* dout, bf16_t* dqkv, const float* rope_cs, void* ws, hipStream_t s);
+
+// ---- padded head layout (64 < d < 128 held in 128-wide slots) -------------------
+// Feature s of a head sits at slot s (s < d/2) or dp/2 + s - d/2; other slots are zero.
+hipError_t pad_head_rows(const bf16_t* src, bf16_t* dst, int heads, int d, int dp, int cols, hipStream_t s);
+hipError_t pad_head_cols(const bf16_t* src, bf16_t* dst, int rows, int heads, int d, int dp, hipStream_t s);
+hipError_t unpad_head_rows(const float* src, float* dst, int heads, int d, int dp, int cols, int accumulate,
+                           hipStream_t s);
+hipError_t unpad_head_cols(const float* src, float* dst, int rows, int heads, int d, int dp, int accumulate,
+                           hipStream_t s);
 
 // ---- token embedding and cross-entropy ------------------------------------------
 // x[t] = E[ids[t]] ([T, H] bf16); an id outside [0, V) gives a NaN row.

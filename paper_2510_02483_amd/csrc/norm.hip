@@ -174,12 +174,12 @@ __global__ __launch_bounds__(64 * SUM_GROUPS) void column_sum_kernel(int parts, 
   }
 }
 
-__global__ void rope_table_kernel(int seq, int head_dim, double theta, float* __restrict__ cs) {
-  const int half = head_dim / 2;
+__global__ void rope_table_kernel(int seq, int head_dim, int table_dim, double theta, float* __restrict__ cs) {
+  const int half = table_dim / 2;
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= (int64_t)seq * half) return;
   const int p = (int)(idx / half), i = (int)(idx % half);
-  const double ang = (double)p * pow(theta, -2.0 * (double)i / (double)head_dim);
+  const double ang = i < head_dim / 2 ? (double)p * pow(theta, -2.0 * (double)i / (double)head_dim) : 0.0;
   cs[idx] = (float)cos(ang);
   cs[(int64_t)seq * half + idx] = (float)sin(ang);
 }
@@ -227,9 +227,11 @@ hipError_t rmsnorm_bwd(int64_t rows, int hidden, const bf16_t* x, const bf16_t* 
   return hipGetLastError();
 }
 
-hipError_t rope_table(int seq, int head_dim, double theta, float* cs, hipStream_t s) {
-  const int64_t n = (int64_t)seq * (head_dim / 2);
-  hipLaunchKernelGGL(rope_table_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, seq, head_dim, theta, cs);
+hipError_t rope_table(int seq, int head_dim, double theta, float* cs, hipStream_t s, int table_dim) {
+  if (table_dim == 0) table_dim = head_dim;
+  const int64_t n = (int64_t)seq * (table_dim / 2);
+  hipLaunchKernelGGL(rope_table_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, seq, head_dim, table_dim,
+                     theta, cs);
   return hipGetLastError();
 }
 

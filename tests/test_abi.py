@@ -54,7 +54,8 @@ def test_query_sizes_tiny():
 
 @pytest.mark.parametrize("field,value,status", [
     ("batch", 0, 2), ("seq", -1, 2), ("hidden", 0, 2), ("n_kv_heads", 3, 2),
-    ("hidden", 260, 2), ("intermediate", 690, 2), ("head_dim", 96, 3), ("head_dim", 32, 3),
+    ("hidden", 260, 2), ("intermediate", 690, 2), ("head_dim", 100, 3), ("head_dim", 32, 3), ("head_dim", 136, 3),
+    ("head_dim", 56, 3),
     ("rope_theta", 1.0, 2), ("rms_eps", -1e-5, 2), ("hidden", 16384, 3),
 ])
 def test_query_sizes_rejects(field, value, status):
@@ -151,7 +152,7 @@ def test_stack_workspace_and_config_checks():
     assert L.ls_stack_workspace(sc.with_(n_layers=0)) < need
     for bad, status in [(dict(vocab=1001), 2), (dict(vocab=0), 2), (dict(n_layers=-1), 2),
                         (dict(vocab=1 << 20, block=c.with_(hidden=512)), 2),
-                        (dict(block=c.with_(head_dim=96)), 3)]:
+                        (dict(block=c.with_(head_dim=100)), 3)]:
         with pytest.raises(L.LsError) as e:
             L.ls_stack_workspace(sc.with_(**bad))
         assert e.value.status == status, bad
@@ -232,3 +233,22 @@ def test_adamw_argument_checks():
     assert lib.ls_adamw_step(100, 50, None, V(p), V(w), V(g), V(m), V(v), None, V(ws), ws_need, None) == 1
     assert lib.ls_adamw_step(100, 50, ctypes.byref(cfg), V(p), None, V(g), V(m), None, None, V(ws), ws_need,
                              None) == 1
+
+
+def test_padded_head_sizes():
+    """head_dim 104 (a 64-head, 6656-wide model) runs in 128-wide slots: the
+    saved q/k/v and o and the workspace hold the padded layout (and padded
+    copies of the projection weights and their fp32 gradients)."""
+    c = configs.TINY.with_(hidden=416, n_q_heads=4, n_kv_heads=2, head_dim=104)
+    s = L.ls_query_sizes(c)
+    T, H = c.tokens, c.hidden
+    pq, pkv = 4 * 128, 2 * 128
+    assert s["attn_saved"] >= 2 * T * (H + pq + 2 * pkv + pq)
+    assert s["attn_workspace"] >= (pq + 2 * pkv) * H * (2 + 4) + H * pq * (2 + 4)
+    s128 = L.ls_query_sizes(c.with_(head_dim=128, hidden=512))
+    assert s128["attn_workspace"] < s["attn_workspace"] + 4 * T * H
+    lib = L.lib()
+    cfg = cfg_of(c)
+    V = ctypes.c_void_p
+    assert lib.ls_attn_core_fwd(ctypes.byref(cfg), V(1 << 32), V(1 << 33), V(1 << 34), None) == 3
+    assert lib.ls_attn_core_bwd_workspace(ctypes.byref(cfg)) == 0

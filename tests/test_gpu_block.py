@@ -20,7 +20,18 @@ MID_D128 = configs.BlockConfig("mid-d128", 6, batch=1, seq=200, hidden=768, n_q_
 MHA_D128 = configs.BlockConfig("mha-d128", 7, batch=2, seq=130, hidden=512, n_q_heads=4, n_kv_heads=4,
                                head_dim=128, intermediate=520, rope_theta=1e4)
 
+# head sizes held in 128-wide slots (104: the report's 30B model; 72: another in-between size)
+D104_GQA = configs.BlockConfig("d104-gqa", 13, batch=2, seq=130, hidden=416, n_q_heads=4, n_kv_heads=2,
+                               head_dim=104, intermediate=520, rope_theta=1e4)
+D104_MHA = configs.BlockConfig("d104-mha", 14, batch=1, seq=200, hidden=624, n_q_heads=6, n_kv_heads=6,
+                               head_dim=104, intermediate=1040, rope_theta=1e4)
+D72 = configs.BlockConfig("d72", 15, batch=2, seq=96, hidden=288, n_q_heads=4, n_kv_heads=1, head_dim=72,
+                          intermediate=392, rope_theta=5e5)
+
 BLOCK_CASES = [
+    ("d104-gqa", D104_GQA, {"gamma": "random"}),
+    ("d104-mha-sharp", D104_MHA, {"wq_std": 0.3}),
+    ("d72", D72, {"gamma": "random"}),
     ("tiny", configs.TINY, {}),
     ("tiny-random-gamma", configs.TINY, {"gamma": "random"}),
     ("tiny-sharp", configs.TINY, {"wq_std": 0.6}),
@@ -213,3 +224,13 @@ def test_block_paper_3b_full_size_prefix():
     c = configs.PAPER_3B
     say(f"paper 3b full size {c}")
     _prefix_parity(c, 768, sample_seq=1)
+
+
+def test_block_paper_30b_full_size_prefix():
+    """The report's own 30B block (Table 1: hidden 6656, 64 heads of 104 in
+    128-wide slots, SwiGLU 17920) at batch 2 x seq 4096; oracle on the first
+    256 tokens of sequence 0."""
+    need_gpu()
+    c = configs.PAPER_30B
+    say(f"paper 30b full size {c}")
+    _prefix_parity(c, 256)
