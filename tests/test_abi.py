@@ -252,3 +252,22 @@ def test_padded_head_sizes():
     V = ctypes.c_void_p
     assert lib.ls_attn_core_fwd(ctypes.byref(cfg), V(1 << 32), V(1 << 33), V(1 << 34), None) == 3
     assert lib.ls_attn_core_bwd_workspace(ctypes.byref(cfg)) == 0
+
+
+def test_size_limits():
+    """Every matrix must stay below 2047 MiB (buffer resources address it with
+    32-bit offsets): the largest shapes are rejected before any HIP call."""
+    big_t = configs.B3.with_(batch=64, seq=8192)           # 512k tokens x 3072 x 2 B = 3 GiB activations
+    with pytest.raises(L.LsError) as e:
+        L.ls_query_sizes(big_t)
+    assert e.value.status == 2 and "2047" in str(e.value)
+    wide = configs.B30.with_(intermediate=163840)          # [T, 2I] gate/up output of 2.5 GiB
+    with pytest.raises(L.LsError) as e:
+        L.ls_query_sizes(wide)
+    assert e.value.status == 2
+    ok = configs.B3.with_(batch=16, seq=2048)               # 32k tokens: 192 MiB activations
+    assert L.ls_query_sizes(ok)["block_workspace"] > 0
+    lib = L.lib()
+    V = ctypes.c_void_p
+    assert lib.ls_cross_entropy(1 << 31, 1, 8, V(1 << 32), V(1 << 33), None, V(1 << 34), V(1 << 35),
+                                V(1 << 36), 1 << 40, None) == 2

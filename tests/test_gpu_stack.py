@@ -233,3 +233,44 @@ def test_stack_paper_3b_full_size_prefix():
     sel[b * S:b * S + t0] = True
     assert np.all(f64(st.row_loss)[~sel] == 0.0)
     compare_stack(st, ref, rows_sel=sel)
+
+
+@pytest.mark.parametrize("case", ["one-token-sequences", "all-ignored"])
+def test_stack_without_targets(case):
+    """Degenerate batches with no row to predict: sequences of one token (the
+    last position has no next token) or every target ignored.  The loss is 0
+    (mean over an empty set taken as 0, as the oracle does) and every
+    gradient is exactly zero."""
+    need_gpu()
+    if case == "one-token-sequences":
+        sc = configs.TINY_STACK.with_(block=configs.TINY_STACK.block.with_(batch=3, seq=1))
+        tg = None
+    else:
+        sc = configs.TINY_STACK
+        tg = torch.full((sc.tokens,), -1, dtype=torch.int32)
+    say(f"stack without targets: {case} {sc}")
+    host = inputs.make_stack_inputs(sc, e_std=0.1, gamma="random")
+    st = L.Stack(sc, host, targets=tg)
+    st.g_arena.fill_(1.0)   # overwritten (accumulate = 0) with exact zeros
+    st.step()
+    torch.cuda.synchronize()
+    ref_loss, ref_rows, _ = oracle_stack(sc, host, targets=tg)
+    assert ref_loss == 0.0 and np.all(ref_rows == 0.0)
+    assert st.loss.item() == 0.0 and torch.count_nonzero(st.row_loss).item() == 0
+    assert torch.count_nonzero(st.g_arena).item() == 0
+
+
+def test_cross_entropy_smallest_vocabulary():
+    """One row of an 8-entry vocabulary (one 16-byte vector: a single lane holds the row)."""
+    need_gpu()
+    z = torch.tensor([[0.5, -1.0, 3.0, 0.0, 2.0, -2.5, 1.0, 0.25]]).to(torch.bfloat16)
+    tg = torch.tensor([4], dtype=torch.int32)
+    rows_ref, loss_ref, dz_ref = ost.cross_entropy(z.double().numpy(), tg.numpy().astype(np.int64))
+    zd = z.cuda()
+    loss = torch.zeros(1, device="cuda")
+    rows = torch.zeros(1, device="cuda")
+    ws = torch.empty(L.ls_cross_entropy_workspace(1), dtype=torch.uint8, device="cuda")
+    L.ls_cross_entropy(zd, 1, tg.cuda(), tg.cuda(), loss, rows, ws)
+    torch.cuda.synchronize()
+    assert abs(loss.item() - loss_ref) < 1e-5 * loss_ref
+    assert max_rel(f64(zd), dz_ref) < OUT_TOL
