@@ -490,8 +490,10 @@ int run_attn_bwd(const ls_block_cfg& cfg, const Dims& m, const bf16_t* x, const 
   return LS_OK;
 }
 
+// keep_gu = false: a forward pass whose saved state is not used (the backward
+// pass recomputes it) skips writing the gate and up outputs.
 int run_mlp_fwd(const ls_block_cfg& cfg, const Dims& m, const bf16_t* x2, const ls_block_weights* w, bf16_t* y,
-                void* saved, hipStream_t st) {
+                void* saved, hipStream_t st, bool keep_gu = true) {
   const MlpSaved sv = mlp_saved_layout(m);
   bf16_t* h2 = at<bf16_t>(saved, sv.h2);
   bf16_t* gu = at<bf16_t>(saved, sv.gu);
@@ -511,7 +513,7 @@ int run_mlp_fwd(const ls_block_cfg& cfg, const Dims& m, const bf16_t* x2, const 
     g.glu_rows = (int)m.I;
     g.ldb = m.H;
     g.epi = ls::EPI_GLU_FWD;
-    g.C = gu;
+    g.C = keep_gu ? gu : nullptr;
     g.ldc = 2 * m.I;
     g.act = act;
     g.glu_I = (int)m.I;
@@ -1063,7 +1065,9 @@ int ls_stack_fwd_bwd(const ls_stack_cfg* cfg, const int32_t* ids, const int32_t*
   for (int l = 0; l < L; ++l) {
     char* sv = set(l);
     if (int e = run_attn_fwd(bc, m, xs(l), &w->layers[l], at<bf16_t>(sv, wl.x2), sv + wl.asv, scratch, st)) return e;
-    if (int e = run_mlp_fwd(bc, m, at<bf16_t>(sv, wl.x2), &w->layers[l], xs(l + 1), sv + wl.msv, st)) return e;
+    if (int e = run_mlp_fwd(bc, m, at<bf16_t>(sv, wl.x2), &w->layers[l], xs(l + 1), sv + wl.msv, st,
+                            !cfg->recompute))
+      return e;
   }
   LS_STEP("rmsnorm fwd", st,
           ls::rmsnorm_fwd(m.T, (int)m.H, bc.rms_eps, xs(L), (const bf16_t*)w->final_norm, hf, rf, st));

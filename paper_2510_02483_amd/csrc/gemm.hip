@@ -531,24 +531,26 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
     // subtiles j = 0, 1 hold gate columns, j = 2, 3 the up columns of the same 64 features
     const int col0 = nw / 2;  // first feature of the wave tile
     const int nvalid = p.glu_I - col0;
+    if (p.C) {  // the gate and up outputs themselves (kept for the backward pass)
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+      for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int j = 0; j < TN; ++j)
+        for (int j = 0; j < TN; ++j)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          float v[4];
+          for (int q = 0; q < 4; ++q) {
+            float v[4];
 #pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * q + e];
-          put4(32 * i + lr, 32 * j + 8 * q + 4 * lh, v);  // [g(64) | u(64)] per row
-        }
+            for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * q + e];
+            put4(32 * i + lr, 32 * j + 8 * q + 4 * lh, v);  // [g(64) | u(64)] per row
+          }
 #pragma unroll 4
-    for (int t = 0; t < 32; ++t) {
-      const int c = lane + 64 * t, r = c >> 4, cc = c & 15;
-      const u32x4 v = *(const u32x4*)&stg[sb(r, cc * 8)];
-      const int f = (cc & 7) * 8;  // feature offset within the 64
-      if (mw + r < p.M && f < nvalid)
-        *(u32x4*)(p.C + (int64_t)(mw + r) * p.ldc + (cc < 8 ? 0 : p.glu_I) + col0 + f) = v;
+      for (int t = 0; t < 32; ++t) {
+        const int c = lane + 64 * t, r = c >> 4, cc = c & 15;
+        const u32x4 v = *(const u32x4*)&stg[sb(r, cc * 8)];
+        const int f = (cc & 7) * 8;  // feature offset within the 64
+        if (mw + r < p.M && f < nvalid)
+          *(u32x4*)(p.C + (int64_t)(mw + r) * p.ldc + (cc < 8 ? 0 : p.glu_I) + col0 + f) = v;
+      }
     }
 #pragma unroll
     for (int i = 0; i < TM; ++i)

@@ -22,7 +22,7 @@ enum Epilogue {
   EPI_BF16 = 0,     // C (bf16) = acc
   EPI_RESID = 1,    // C (bf16) = acc + R
   EPI_ROPE = 2,     // C (bf16) = rotate(acc) on columns < rope_cols, acc elsewhere
-  EPI_GLU_FWD = 3,  // gu[m][i] = g, gu[m][I+i] = u, act[m][i] = silu(g) u
+  EPI_GLU_FWD = 3,  // gu[m][i] = g, gu[m][I+i] = u (C; skipped when null), act[m][i] = silu(g) u
   EPI_GLU_BWD = 4,  // C = dgu: dgu[m][i] = acc u silu'(g), dgu[m][I+i] = acc silu(g)
   EPI_F32 = 5,      // F (fp32, rows split over up to three buffers) (+)= acc
 };
