@@ -4,7 +4,10 @@
  * The library computes the forward and backward pass of one Llama-style
  * decoder block, the part of a transformer whose attention and MLP layers the
  * Litespark report (arXiv 2510.02483) speeds up (Section 1) while keeping the
- * standard block's result (abstract, Section 5).  The block is the one the
+ * standard block's result (abstract, Section 5).  Around it: the whole model's
+ * forward and backward pass (token embedding, a stack of blocks, final
+ * RMSNorm, tied LM head, next-token cross-entropy) and the optimizer step
+ * (global-norm clipping and AdamW) of the report's training setup.  The block is the one the
  * report's Section 2.4 describes: pre-norm RMSNorm, rotary position embedding,
  * causal grouped-query attention (multi-head when kv heads = query heads) and
  * a SwiGLU MLP, with residual adds:
