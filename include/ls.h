@@ -174,6 +174,9 @@ typedef struct {
   int32_t recompute;  /* 1: keep only each block's input in the forward pass and
                          recompute the block's saved state in the backward pass;
                          0: keep every block's saved state (more workspace) */
+  int32_t logits_chunk; /* token rows whose logits are formed at a time: 0 = as
+                           many as stay below 2047 MiB of bf16 logits; a smaller
+                           positive value trades workspace for more launches */
 } ls_stack_cfg;
 
 /* embed [vocab, hidden] bf16 (input embedding and LM head); final_norm

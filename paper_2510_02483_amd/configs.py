@@ -79,6 +79,7 @@ class StackConfig:
     n_layers: int
     vocab: int
     recompute: bool = True  # keep only block inputs; recompute each block in the backward
+    logits_chunk: int = 0   # token rows of logits formed at a time (0: as many as fit one 2047 MiB operand)
 
     @property
     def tokens(self) -> int:

@@ -634,17 +634,20 @@ int check_stack_cfg(const ls_stack_cfg* c) {
   if (c->n_layers < 0 || c->n_layers > 4096) return fail(LS_ERR_SHAPE, "n_layers %d out of range [0, 4096]", c->n_layers);
   if (c->vocab <= 0 || c->vocab % 8 != 0) return fail(LS_ERR_SHAPE, "vocab (%d) must be a positive multiple of 8", c->vocab);
   if (c->recompute != 0 && c->recompute != 1) return fail(LS_ERR_SHAPE, "recompute must be 0 or 1");
+  if (c->logits_chunk < 0) return fail(LS_ERR_SHAPE, "logits_chunk must be >= 0");
   if ((int64_t)c->vocab * c->block.hidden * 4 >= kMaxBytes)
     return fail(LS_ERR_SHAPE, "vocab x hidden fp32 gradient reaches 2047 MiB");
   return LS_OK;
 }
 
 // Token rows per logits chunk: the [rows, vocab] bf16 logits of one chunk stay
-// below the 2047 MiB limit of one matrix-product operand.
+// below the 2047 MiB limit of one matrix-product operand (and within the
+// caller's logits_chunk when set).
 int64_t logits_rows(const ls_stack_cfg& c) {
   const Dims m = dims_of(c.block);
   int64_t per = (kMaxBytes - 1) / ((int64_t)c.vocab * 2);
   if (per >= 256) per &= ~(int64_t)255;
+  if (c.logits_chunk > 0) per = std::min<int64_t>(per, c.logits_chunk);
   return std::min<int64_t>(m.T, per);
 }
 

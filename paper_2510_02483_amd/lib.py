@@ -49,7 +49,7 @@ class LsSizes(ctypes.Structure):
 
 class LsStackCfg(ctypes.Structure):
     _fields_ = [("block", LsBlockCfg), ("n_layers", ctypes.c_int32), ("vocab", ctypes.c_int32),
-                ("recompute", ctypes.c_int32)]
+                ("recompute", ctypes.c_int32), ("logits_chunk", ctypes.c_int32)]
 
 
 class LsStackWeights(ctypes.Structure):
@@ -249,7 +249,7 @@ def ls_gemm_tn(A, B, C, accumulate=False, stream=None):
 
 
 def make_stack_cfg(sc: StackConfig) -> LsStackCfg:
-    return LsStackCfg(make_cfg(sc.block), sc.n_layers, sc.vocab, int(sc.recompute))
+    return LsStackCfg(make_cfg(sc.block), sc.n_layers, sc.vocab, int(sc.recompute), int(sc.logits_chunk))
 
 
 def ls_stack_workspace(sc: StackConfig) -> int:

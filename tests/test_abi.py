@@ -157,6 +157,11 @@ def test_stack_workspace_and_config_checks():
             L.ls_stack_workspace(sc.with_(**bad))
         assert e.value.status == status, bad
     lib = L.lib()
+    assert L.ls_stack_workspace(sc.with_(logits_chunk=40)) < need, "smaller logits chunks need less workspace"
+    cfg = L.make_stack_cfg(sc)
+    cfg.logits_chunk = -1
+    n0 = ctypes.c_size_t(0)
+    assert L.lib().ls_stack_workspace(ctypes.byref(cfg), ctypes.byref(n0)) == 2
     cfg = L.make_stack_cfg(sc)
     cfg.recompute = 2
     n = ctypes.c_size_t(0)

@@ -155,6 +155,22 @@ def test_stack_tiny(recompute):
     compare_stack(st, oracle_stack(sc, host), scale=2.0)
 
 
+def test_stack_logits_in_chunks():
+    """Logits formed 40 token rows at a time (4 chunks, the last one ragged):
+    the head's gradient accumulates over the chunks; same results as the
+    oracle.  Heads of 104 features (padded slots) in the blocks."""
+    need_gpu()
+    blk = configs.BlockConfig("stack-d104", 17, batch=2, seq=64, hidden=416, n_q_heads=4, n_kv_heads=4,
+                              head_dim=104, intermediate=520, rope_theta=1e4)
+    sc = configs.StackConfig("stack-chunks", blk, n_layers=2, vocab=1000, logits_chunk=40)
+    say(f"stack {sc}")
+    host = inputs.make_stack_inputs(sc, gamma="random", e_std=0.1)
+    st = L.Stack(sc, host)
+    st.step()
+    torch.cuda.synchronize()
+    compare_stack(st, oracle_stack(sc, host))
+
+
 def test_stack_tiny_explicit_targets_and_depth():
     """Explicit targets with ignored rows, three blocks, d = 128 heads."""
     need_gpu()
