@@ -325,8 +325,10 @@ PaddedWeights padded_weights(const Dims& m, const ls_block_weights* w, void* ws,
   return {wp, wp + m.Pq * m.H, wp + (m.Pq + m.Pkv) * m.H, wo, LS_OK};
 }
 
+// out_proj = false: stop after the attention core (a recomputation whose x2 is
+// already known).
 int run_attn_fwd(const ls_block_cfg& cfg, const Dims& m, const bf16_t* x, const ls_block_weights* w, bf16_t* x2,
-                 void* saved, void* ws, hipStream_t st) {
+                 void* saved, void* ws, hipStream_t st, bool out_proj = true) {
   const AttnSaved sv = attn_saved_layout(m);
   const AttnWs wl = attn_ws_layout(m);
   bf16_t* h1 = at<bf16_t>(saved, sv.h1);
@@ -360,6 +362,7 @@ int run_attn_fwd(const ls_block_cfg& cfg, const Dims& m, const bf16_t* x, const 
   g.rope_cols = (int)(m.Pq + m.Pkv);
   LS_STEP("qkv projection", st, ls::gemm(g, st));
   LS_STEP("attention fwd", st, ls::attn_fwd(attn_shape(m), qkv, o, lse, st));
+  if (!out_proj) return LS_OK;
   ls::GemmArgs p;
   p.M = (int)m.T;
   p.N = (int)m.H;
@@ -491,9 +494,10 @@ int run_attn_bwd(const ls_block_cfg& cfg, const Dims& m, const bf16_t* x, const 
 }
 
 // keep_gu = false: a forward pass whose saved state is not used (the backward
-// pass recomputes it) skips writing the gate and up outputs.
+// pass recomputes it) skips writing the gate and up outputs.  down = false:
+// stop before the down projection (a recomputation whose y is already known).
 int run_mlp_fwd(const ls_block_cfg& cfg, const Dims& m, const bf16_t* x2, const ls_block_weights* w, bf16_t* y,
-                void* saved, hipStream_t st, bool keep_gu = true) {
+                void* saved, hipStream_t st, bool keep_gu = true, bool down = true) {
   const MlpSaved sv = mlp_saved_layout(m);
   bf16_t* h2 = at<bf16_t>(saved, sv.h2);
   bf16_t* gu = at<bf16_t>(saved, sv.gu);
@@ -519,6 +523,7 @@ int run_mlp_fwd(const ls_block_cfg& cfg, const Dims& m, const bf16_t* x2, const 
     g.glu_I = (int)m.I;
     LS_STEP("gate/up projection", st, ls::gemm(g, st));
   }
+  if (!down) return LS_OK;
   {
     ls::GemmArgs g;
     g.M = (int)m.T;
@@ -652,7 +657,7 @@ int64_t logits_rows(const ls_stack_cfg& c) {
 }
 
 struct StackWs {
-  size_t tg, counts, rows, xs, hf, rf, logits, dh, dxa, dxb, ysink, partial, sets, set_stride, dx2, scratch, total;
+  size_t tg, counts, rows, xs, xmid, hf, rf, logits, dh, dxa, dxb, partial, sets, set_stride, dx2, scratch, total;
   size_t asv, msv, x2;  // offsets inside one set
 };
 StackWs stack_ws_layout(const ls_stack_cfg& c) {
@@ -664,13 +669,15 @@ StackWs stack_ws_layout(const ls_stack_cfg& c) {
   w.counts = k.take(16);
   w.rows = k.take(m.T * 4);
   w.xs = k.take(act * (size_t)(c.n_layers + 1));
+  // with recomputation each block's mid-residual x2 is kept too, so that the
+  // recomputation stops before the output and down projections
+  w.xmid = k.take(c.recompute ? act * (size_t)c.n_layers : 0);
   w.hf = k.take(act);
   w.rf = k.take(m.T * 4);
   w.logits = k.take((size_t)logits_rows(c) * c.vocab * 2);
   w.dh = k.take(act);
   w.dxa = k.take(act);
   w.dxb = k.take(act);
-  w.ysink = k.take(c.recompute ? act : 0);
   w.partial = k.take(norm_partial_bytes(m));
   w.dx2 = k.take(act);
   w.scratch = k.take(std::max(attn_ws_layout(m).total, mlp_ws_layout(m).total));
@@ -1065,12 +1072,14 @@ int ls_stack_fwd_bwd(const ls_stack_cfg* cfg, const int32_t* ids, const int32_t*
 
   // forward: embedding, blocks (keeping every block's input), final norm
   LS_STEP("embedding fwd", st, ls::embed_fwd(m.T, (int)m.H, (int)V, ids, E, xs(0), st));
+  // a block's mid-residual x2: kept per block with recomputation, else in the block's saved set
+  auto x2_of = [&](int l) {
+    return cfg->recompute ? at<bf16_t>(workspace, wl.xmid + act * (size_t)l) : at<bf16_t>(set(l), wl.x2);
+  };
   for (int l = 0; l < L; ++l) {
     char* sv = set(l);
-    if (int e = run_attn_fwd(bc, m, xs(l), &w->layers[l], at<bf16_t>(sv, wl.x2), sv + wl.asv, scratch, st)) return e;
-    if (int e = run_mlp_fwd(bc, m, at<bf16_t>(sv, wl.x2), &w->layers[l], xs(l + 1), sv + wl.msv, st,
-                            !cfg->recompute))
-      return e;
+    if (int e = run_attn_fwd(bc, m, xs(l), &w->layers[l], x2_of(l), sv + wl.asv, scratch, st)) return e;
+    if (int e = run_mlp_fwd(bc, m, x2_of(l), &w->layers[l], xs(l + 1), sv + wl.msv, st, !cfg->recompute)) return e;
   }
   LS_STEP("rmsnorm fwd", st,
           ls::rmsnorm_fwd(m.T, (int)m.H, bc.rms_eps, xs(L), (const bf16_t*)w->final_norm, hf, rf, st));
@@ -1139,10 +1148,10 @@ int ls_stack_fwd_bwd(const ls_stack_cfg* cfg, const int32_t* ids, const int32_t*
                           acc, at<float>(workspace, wl.partial), st));
   for (int l = L - 1; l >= 0; --l) {
     char* sv = set(l);
-    bf16_t* x2 = at<bf16_t>(sv, wl.x2);
-    if (cfg->recompute) {
-      if (int e = run_attn_fwd(bc, m, xs(l), &w->layers[l], x2, sv + wl.asv, scratch, st)) return e;
-      if (int e = run_mlp_fwd(bc, m, x2, &w->layers[l], at<bf16_t>(workspace, wl.ysink), sv + wl.msv, st)) return e;
+    bf16_t* x2 = x2_of(l);
+    if (cfg->recompute) {  // the saved state of both sub-layers; x2 and y are known
+      if (int e = run_attn_fwd(bc, m, xs(l), &w->layers[l], x2, sv + wl.asv, scratch, st, false)) return e;
+      if (int e = run_mlp_fwd(bc, m, x2, &w->layers[l], nullptr, sv + wl.msv, st, true, false)) return e;
     }
     if (int e = run_mlp_bwd(bc, m, x2, &w->layers[l], sv + wl.msv, dcur, dx2, &g->layers[l], acc, scratch, st))
       return e;
