@@ -63,7 +63,7 @@ void timing_mark(const char* label, hipStream_t st, bool start) {
   if (!g_timing.armed || g_timing.label != label) return;
   const size_t idx = 2 * (size_t)g_timing.used + (start ? 0 : 1);
   if (idx >= g_timing.ev.size()) return;
-  hipEventRecord(g_timing.ev[idx], st);
+  (void)hipEventRecord(g_timing.ev[idx], st);
   if (!start) ++g_timing.used;
 }
 
@@ -823,14 +823,14 @@ int ls_timing_begin(const char* label, int max_launches) {
   if (!label) return fail(LS_ERR_NULL, "label is NULL");
   if (max_launches <= 0 || max_launches > 100000) return fail(LS_ERR_SHAPE, "max_launches out of range");
   std::lock_guard<std::mutex> lk(g_timing.mu);
-  for (hipEvent_t e : g_timing.ev) hipEventDestroy(e);
+  for (hipEvent_t e : g_timing.ev) (void)hipEventDestroy(e);
   g_timing.ev.clear();
   g_timing.armed = false;
   for (int i = 0; i < 2 * max_launches; ++i) {
     hipEvent_t e;
     hipError_t r = hipEventCreate(&e);
     if (r != hipSuccess) {
-      for (hipEvent_t x : g_timing.ev) hipEventDestroy(x);
+      for (hipEvent_t x : g_timing.ev) (void)hipEventDestroy(x);
       g_timing.ev.clear();
       return hip_fail(r, "hipEventCreate");
     }
@@ -856,7 +856,7 @@ int ls_timing_end(int* launches, float* mean_ms) {
     if (r != hipSuccess) rc = hip_fail(r, "timing events");
     total += ms;
   }
-  for (hipEvent_t e : g_timing.ev) hipEventDestroy(e);
+  for (hipEvent_t e : g_timing.ev) (void)hipEventDestroy(e);
   g_timing.ev.clear();
   g_timing.used = 0;
   *launches = n;
