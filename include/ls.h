@@ -206,9 +206,9 @@ int ls_stack_workspace(const ls_stack_cfg* cfg, size_t* bytes);
  * target).  Errors reported through the result rather than the status (the
  * library never reads ids on the host): an id outside [0, vocab) makes its
  * embedding row NaN, and a target outside [-1, vocab) makes its row's loss
- * and gradient NaN; neither reads or writes outside any buffer.  The
- * embedding gradient adds repeated tokens with fp32 atomics, so its low bits
- * can differ between runs; every other output is deterministic. */
+ * and gradient NaN; neither reads or writes outside any buffer.  Every
+ * output is deterministic (the embedding gradient sums repeated tokens in
+ * token order). */
 int ls_stack_fwd_bwd(const ls_stack_cfg* cfg, const int32_t* ids, const int32_t* targets,
                      const ls_stack_weights* w, float* loss, float* row_loss,
                      const ls_stack_grads* g, int accumulate, void* workspace,
@@ -305,7 +305,9 @@ int ls_cross_entropy(int64_t tokens, int32_t seq, int32_t vocab, ls_bf16* logits
 
 /* Token embedding rows: x[t] = embed[ids[t]] ([tokens, hidden] bf16; an id
  * outside [0, vocab) gives a NaN row), and its backward, which ADDS dx[t] into
- * d_embed[ids[t]] (fp32; ids outside [0, vocab) skipped). */
+ * d_embed[ids[t]] (fp32; the rows of repeated ids summed in token order, so
+ * the result is deterministic; ids outside [0, vocab) skipped; hidden at most
+ * 8192 for the backward). */
 int ls_embed_fwd(int64_t tokens, int32_t hidden, int32_t vocab, const int32_t* ids,
                  const ls_bf16* embed, ls_bf16* x, void* stream);
 int ls_embed_bwd(int64_t tokens, int32_t hidden, int32_t vocab, const int32_t* ids,

@@ -1207,6 +1207,8 @@ int ls_embed_bwd(int64_t tokens, int32_t hidden, int32_t vocab, const int32_t* i
                  void* stream) {
   if (tokens <= 0 || hidden <= 0 || hidden % 8 != 0 || vocab <= 0)
     return fail(LS_ERR_SHAPE, "tokens, vocab must be positive and hidden a positive multiple of 8");
+  if (hidden > 8192) return fail(LS_ERR_UNSUPPORTED, "hidden %d exceeds 8192", hidden);
+  if (tokens >= ((int64_t)1 << 31)) return fail(LS_ERR_SHAPE, "tokens (%lld) reaches 2^31", (long long)tokens);
   std::vector<Range> in{{ids, (size_t)tokens * 4, "ids"}, {dx, (size_t)(tokens * hidden * 2), "dx"}};
   std::vector<Range> out{{d_embed, (size_t)vocab * hidden * 4, "d_embed"}};
   if (int e = check_ranges(in, out)) return e;

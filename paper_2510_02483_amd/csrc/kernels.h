@@ -97,7 +97,8 @@ hipError_t unpad_head_cols(const float* src, float* dst, int rows, int heads, in
 // ---- token embedding and cross-entropy ------------------------------------------
 // x[t] = E[ids[t]] ([T, H] bf16); an id outside [0, V) gives a NaN row.
 hipError_t embed_fwd(int64_t T, int H, int V, const int32_t* ids, const bf16_t* E, bf16_t* x, hipStream_t s);
-// dE[ids[t]] += dx[t] (fp32 atomics; ids outside [0, V) skipped).
+// dE[ids[t]] += dx[t], repeated ids summed in token order (deterministic; ids
+// outside [0, V) skipped).  H a multiple of 8, at most 8192.
 hipError_t embed_bwd(int64_t T, int H, int V, const int32_t* ids, const bf16_t* dx, float* dE, hipStream_t s);
 // tg[t] = targets[t], or (targets null) ids[t+1] within a sequence of S tokens
 // and -1 at its last position; counts[0] = rows with a target in [0, V).

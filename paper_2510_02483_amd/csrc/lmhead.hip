@@ -1,4 +1,4 @@
-// Token embedding (row gather and its scatter-add backward) and the softmax
+// Token embedding (row gather and its deterministic scatter-add backward) and the softmax
 // cross-entropy over rows of vocabulary logits, with its gradient written in
 // place of the logits.
 //
@@ -37,24 +37,78 @@ __global__ __launch_bounds__(256) void embed_fwd_kernel(int64_t T, int H, int V,
   for (int c = lane; c < H / 8; c += 64) dst[c] = ok ? src[c] : nan4;
 }
 
-// dE[ids[t]] += dx[t] (fp32 atomic adds; rows with an id outside [0, V) are
-// skipped).  Repeated ids add in an unspecified order.
-__global__ __launch_bounds__(256) void embed_bwd_kernel(int64_t T, int H, int V, const int32_t* __restrict__ ids,
-                                                        const bf16_t* __restrict__ dx, float* __restrict__ dE) {
-  const int lane = threadIdx.x & 63;
-  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= T) return;
+// dE[ids[t]] += dx[t], deterministically: workgroup t handles token t, and
+// only if t is the first occurrence of its id; it then sums the dx rows of
+// every occurrence in increasing token order and adds the sum into the id's
+// row with one plain read-modify-write (no other workgroup touches that row).
+// Occurrences are found by comparing ids 64 at a time (a ballot per wave), so
+// the scan costs O(T) id reads per token, all L2-resident.  Rows with an id
+// outside [0, V) are skipped.  hidden <= 8192.
+constexpr int EMB_THREADS = 256;
+constexpr int EMB_CHUNKS = 4;  // 8-column chunks per thread (hidden / 8 <= 4 * 256)
+
+__global__ __launch_bounds__(EMB_THREADS) void embed_bwd_kernel(int64_t T, int H, int V,
+                                                               const int32_t* __restrict__ ids,
+                                                               const bf16_t* __restrict__ dx,
+                                                               float* __restrict__ dE) {
+  __shared__ unsigned long long match[EMB_THREADS / 64];
+  const int64_t t = blockIdx.x;
   const int id = ids[t];
   if (id < 0 || id >= V) return;
-  float* dst = dE + (int64_t)id * H;
-  const u32x4* src = (const u32x4*)(dx + t * H);
-  for (int c = lane; c < H / 8; c += 64) {
-    const u32x4 w = src[c];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // an earlier occurrence owns the row
+  int earlier = 0;
+  for (int64_t j = tid; j < t; j += EMB_THREADS) earlier |= ids[j] == id;
+  if (__syncthreads_or(earlier)) return;
+  const int nch = H / 8;
+  float acc[EMB_CHUNKS][8];
+#pragma unroll
+  for (int r = 0; r < EMB_CHUNKS; ++r) {
+    const int c = tid + EMB_THREADS * r;
+    u32x4 w = c < nch ? *(const u32x4*)(dx + t * H + 8 * c) : u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      unsafeAtomicAdd(dst + 8 * c + 2 * e, bf_lo(w[e]));
-      unsafeAtomicAdd(dst + 8 * c + 2 * e + 1, bf_hi(w[e]));
+      acc[r][2 * e] = bf_lo(w[e]);
+      acc[r][2 * e + 1] = bf_hi(w[e]);
     }
+  }
+  // later occurrences, 256 ids per round, added in token order
+  for (int64_t j0 = t + 1; j0 < T; j0 += EMB_THREADS) {
+    const int64_t j = j0 + tid;
+    const unsigned long long m = __ballot(j < T && ids[j] == id);
+    if (lane == 0) match[wave] = m;
+    __syncthreads();
+#pragma unroll
+    for (int w = 0; w < EMB_THREADS / 64; ++w) {
+      unsigned long long mw = match[w];
+      while (mw) {
+        const int b = __builtin_ctzll(mw);
+        mw &= mw - 1;
+        const int64_t row = j0 + 64 * w + b;
+#pragma unroll
+        for (int r = 0; r < EMB_CHUNKS; ++r) {
+          const int c = tid + EMB_THREADS * r;
+          if (c >= nch) continue;
+          const u32x4 x = *(const u32x4*)(dx + row * H + 8 * c);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            acc[r][2 * e] += bf_lo(x[e]);
+            acc[r][2 * e + 1] += bf_hi(x[e]);
+          }
+        }
+      }
+    }
+    __syncthreads();
+  }
+  float* dst = dE + (int64_t)id * H;
+#pragma unroll
+  for (int r = 0; r < EMB_CHUNKS; ++r) {
+    const int c = tid + EMB_THREADS * r;
+    if (c >= nch) continue;
+    f32x4* d4 = (f32x4*)(dst + 8 * c);
+    const f32x4 a = d4[0], b = d4[1];
+    d4[0] = f32x4{a[0] + acc[r][0], a[1] + acc[r][1], a[2] + acc[r][2], a[3] + acc[r][3]};
+    d4[1] = f32x4{b[0] + acc[r][4], b[1] + acc[r][5], b[2] + acc[r][6], b[3] + acc[r][7]};
   }
 }
 
@@ -234,7 +288,8 @@ hipError_t embed_fwd(int64_t T, int H, int V, const int32_t* ids, const bf16_t* 
 
 hipError_t embed_bwd(int64_t T, int H, int V, const int32_t* ids, const bf16_t* dx, float* dE, hipStream_t s) {
   if (T <= 0) return hipSuccess;
-  embed_bwd_kernel<<<dim3((unsigned)((T + 3) / 4)), dim3(256), 0, s>>>(T, H, V, ids, dx, dE);
+  if (H % 8 != 0 || H / 8 > EMB_CHUNKS * EMB_THREADS || T >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
+  embed_bwd_kernel<<<dim3((unsigned)T), dim3(EMB_THREADS), 0, s>>>(T, H, V, ids, dx, dE);
   return hipGetLastError();
 }
 
