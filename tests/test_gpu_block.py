@@ -79,11 +79,13 @@ def test_block_parity(name, c, kw):
     compare_block(c, blk, fwd, gr)
 
 
-def test_sublayers_match_block_call():
+@pytest.mark.parametrize("c", [MID_D64, D104_GQA], ids=["d64", "d104-padded"])
+def test_sublayers_match_block_call(c):
     """ls_attn_fwd / ls_mlp_fwd / ls_mlp_bwd / ls_attn_bwd chained by hand give
-    the oracle's intermediates (x2, dx2) and final results."""
+    the oracle's intermediates (x2, dx2) and final results (also with heads of
+    104 in padded slots, whose saved state and workspace the separate calls
+    pass between them)."""
     need_gpu()
-    c = MID_D64
     say(f"sub-layers {c}")
     host = inputs.make_inputs(c, gamma="random")
     dev = {k: v.cuda() for k, v in host.items()}
@@ -101,6 +103,7 @@ def test_sublayers_match_block_call():
     L.ls_attn_fwd(c, x, w, x2, asv, aws)
     L.ls_mlp_fwd(c, x2, w, y, msv, mws)
     L.ls_mlp_bwd(c, x2, w, msv, dy, dx2, g, False, mws)
+    aws.fill_(255)  # the backward rebuilds whatever it needs in its workspace
     L.ls_attn_bwd(c, x, w, asv, dx2, dx, g, False, aws)
     torch.cuda.synchronize()
     fwd, gr = oracle_block(c, inputs.to_f64(host))
