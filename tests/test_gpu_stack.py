@@ -160,6 +160,18 @@ def test_stack_tiny(recompute):
     compare_stack(st, oracle_stack(sc, host), scale=2.0)
 
 
+def test_stack_without_blocks():
+    """Zero blocks: embedding, final RMSNorm, tied head and loss alone."""
+    need_gpu()
+    sc = configs.TINY_STACK.with_(n_layers=0)
+    say(f"stack {sc}")
+    host = inputs.make_stack_inputs(sc, gamma="random", e_std=0.5)
+    st = L.Stack(sc, host)
+    st.step()
+    torch.cuda.synchronize()
+    compare_stack(st, oracle_stack(sc, host))
+
+
 def test_stack_logits_in_chunks():
     """Logits formed 40 token rows at a time (4 chunks, the last one ragged):
     the head's gradient accumulates over the chunks; same results as the
