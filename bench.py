@@ -272,7 +272,7 @@ def main():
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU only: this build runs the block on a single MI355X "
+        print("bench.py measures one GPU only: the library runs on a single MI355X "
               "(no sharding or collectives); run it with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
