@@ -329,7 +329,11 @@ LS_DEV void unrotate_store(const f32x16 (&acc)[D / 32], float scale, const float
 
 // dK and dV for 128 keys of one kv head (4 waves x 32 keys), summed over the
 // query heads of the group, no atomics.  The 1-D grid runs the key tiles with
-// the most queries after them (lowest key index) first.
+// the most queries after them (lowest key index) first.  With few kv heads
+// (and so few workgroups) the group's query heads are split over `hsplit`
+// workgroups, each of which writes its fp32 partial sums to `part`
+// ([hsplit][batch*seq][nkv][dK | dV]); attn_bwd_dkdv_reduce then adds the
+// partials in a fixed order and stores dK and dV.
 //
 // A wave issues one MFMA per slot.  Each 32-query block of a 64-query tile
 // takes four phases: S = Q K^T, dP = dO V^T, dV^T += dO^T P, dK^T += Q^T dS.
@@ -341,13 +345,13 @@ LS_DEV void unrotate_store(const f32x16 (&acc)[D / 32], float scale, const float
 // slots before the end of tile t each wave waits for its loads of tile t+1
 // and for the other waves (whose reads of tile t-1 are then done), and the
 // loads of tile t+2 go into tile t-1's stage.
-template <int D>
+template <int D, bool SPLIT>
 __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnShape sh, const bf16_t* __restrict__ qkv,
                                                                 const bf16_t* __restrict__ dout,
                                                                 const float* __restrict__ lse2,
                                                                 const float* __restrict__ Dv, bf16_t* __restrict__ dqkv,
                                                                 const float* __restrict__ rope_cs, float scale,
-                                                                float sl2) {
+                                                                float sl2, int hsplit_arg, float* __restrict__ part) {
   constexpr int NST = 3;                    // LDS stages
   constexpr int NSD = D / 16, NI = D / 32;  // 16-wide d steps; 32-row d blocks
   constexpr int P1 = NSD, P2 = NSD, P3 = 2 * NI, P4 = 2 * NI;  // slots per phase
@@ -367,9 +371,11 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnShape sh, con
   };
   __shared__ __attribute__((aligned(1024))) Stage stg[NST];
 
-  const int S = sh.seq, nq = sh.nq, nkv = sh.nkv, G = nq / nkv;
-  const int per = nkv * sh.batch, x = (int)blockIdx.x;
-  const int kvt = x / per, kvh = (x % per) % nkv, b = (x % per) / nkv;
+  const int hsplit = SPLIT ? hsplit_arg : 1;  // the unsplit instance folds every split term away
+  const int S = sh.seq, nq = sh.nq, nkv = sh.nkv, G = nq / nkv, Gs = SPLIT ? G / hsplit : G;
+  const int per = nkv * sh.batch * hsplit, x = (int)blockIdx.x;
+  const int kvt = x / per, hs = (x % per) % hsplit, kvh = ((x % per) / hsplit) % nkv,
+            b = ((x % per) / hsplit) / nkv;
   const int64_t ld = (int64_t)(nq + 2 * nkv) * D;
   const int64_t ldo = (int64_t)nq * D;
   const bf16_t* base = qkv + (int64_t)b * S * ld;
@@ -381,12 +387,12 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnShape sh, con
   const int kv0 = kvt * BWD_BKV;
   const int kvrow = kv0 + 32 * wave + lr;
 
-  // tiles t = 0 .. G*nqt-1: query head kvh*G + t/nqt, queries q_begin + (t%nqt)*BWD_BQ ..
+  // tiles t = 0 .. Gs*nqt-1: query head kvh*G + hs*Gs + t/nqt, queries q_begin + (t%nqt)*BWD_BQ ..
   const int q_begin = kv0;  // earlier queries see none of these keys
   const int nqt = (S - q_begin + BWD_BQ - 1) / BWD_BQ;
-  const int ntiles = G * nqt;
+  const int ntiles = Gs * nqt;
   auto issue = [&](int t, int st) {
-    const int h = kvh * G + t / nqt, q0 = q_begin + (t % nqt) * BWD_BQ;
+    const int h = kvh * G + hs * Gs + t / nqt, q0 = q_begin + (t % nqt) * BWD_BQ;
     load_tile<D, BWD_BQ, true>(rq_, ld, q0, S, h * D, stg[st].q, wave, lane);
     load_tile<D, BWD_BQ, true>(rdo, ldo, q0, S, h * D, stg[st].o, wave, lane);
     if (wave == 0) load_vec64(rsrc(lse2 + ((int64_t)b * nq + h) * S, (uint32_t)S * 4), q0, S, stg[st].l, lane);
@@ -503,8 +509,79 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnShape sh, con
 
   // dK = scale * dS^T Q (un-rotated), dV = P^T dO.  Lane holds key kvrow.
   if (kvrow >= S) return;
-  unrotate_store<D>(dk, scale, rope_cs, S, kvrow, lh, dqkv + ((int64_t)b * S + kvrow) * ld + (nq + kvh) * D);
-  unrotate_store<D>(dv, 1.0f, nullptr, S, kvrow, lh, dqkv + ((int64_t)b * S + kvrow) * ld + (nq + nkv + kvh) * D);
+  if constexpr (SPLIT) {  // partial sums of this workgroup's heads; lane holds columns 32i + 8(r/4) + 4lh + r%4
+    float* row = part + (((int64_t)hs * sh.batch * S + (int64_t)b * S + kvrow) * nkv + kvh) * (2 * D);
+#pragma unroll
+    for (int i = 0; i < NI; ++i)
+#pragma unroll
+      for (int rq = 0; rq < 4; ++rq) {
+        const int c = 32 * i + 8 * rq + 4 * lh;
+        *(f32x4*)(row + c) = f32x4{dk[i][4 * rq], dk[i][4 * rq + 1], dk[i][4 * rq + 2], dk[i][4 * rq + 3]};
+        *(f32x4*)(row + D + c) = f32x4{dv[i][4 * rq], dv[i][4 * rq + 1], dv[i][4 * rq + 2], dv[i][4 * rq + 3]};
+      }
+  } else {
+    unrotate_store<D>(dk, scale, rope_cs, S, kvrow, lh, dqkv + ((int64_t)b * S + kvrow) * ld + (nq + kvh) * D);
+    unrotate_store<D>(dv, 1.0f, nullptr, S, kvrow, lh, dqkv + ((int64_t)b * S + kvrow) * ld + (nq + nkv + kvh) * D);
+  }
+}
+
+// Sum of the hsplit partial dK / dV rows of attn_bwd_dkdv_kernel, in split
+// order, then scale and inverse RoPE for dK, bf16 stores into dqkv.  One wave
+// per (token, kv head): lane l holds columns 4l .. 4l+3 of [dK | dV] (D = 128)
+// or 2l .. 2l+1 (D = 64); the RoPE partner of dK column c < D/2 is c + D/2.
+template <int D>
+__global__ __launch_bounds__(256) void attn_bwd_dkdv_reduce(AttnShape sh, int hsplit, const float* __restrict__ part,
+                                                            bf16_t* __restrict__ dqkv, const float* __restrict__ rope_cs,
+                                                            float scale) {
+  constexpr int E = 2 * D / 64;  // columns per lane
+  constexpr int HALF = D / 2;
+  const int lane = threadIdx.x & 63;
+  const int64_t T = (int64_t)sh.batch * sh.seq;
+  const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);  // (token, kv head)
+  if (w >= T * sh.nkv) return;
+  const int64_t t = w / sh.nkv;
+  const int kvh = (int)(w % sh.nkv), pos = (int)(t % sh.seq);
+  const int c0 = E * lane;  // first of this lane's columns in [dK | dV]
+  float v[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) v[e] = 0.f;
+  for (int hs = 0; hs < hsplit; ++hs) {
+    const float* src = part + ((int64_t)hs * T * sh.nkv + w) * (2 * D) + c0;
+    if constexpr (E == 4) {
+      const f32x4 a = *(const f32x4*)src;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] += a[e];
+    } else {
+      const float2 a = *(const float2*)src;
+      v[0] += a.x;
+      v[1] += a.y;
+    }
+  }
+  const bool is_k = c0 < D;
+  // partner columns of dK (c0 +- D/2): lanes HALF/E apart
+  float pv[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) pv[e] = __shfl_xor(v[e], HALF / E);
+  const int64_t ld = (int64_t)(sh.nq + 2 * sh.nkv) * D;
+  bf16_t* row = dqkv + t * ld + (int64_t)(sh.nq + (is_k ? 0 : sh.nkv) + kvh) * D;
+  const int d0 = is_k ? c0 : c0 - D;
+  float out[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    if (!is_k) {
+      out[e] = v[e];
+    } else if (!rope_cs) {
+      out[e] = v[e] * scale;
+    } else {
+      const int d = d0 + e, i = d % HALF;
+      const float cs = rope_cs[(int64_t)pos * HALF + i];
+      const float sn = rope_cs[(int64_t)sh.seq * HALF + (int64_t)pos * HALF + i];
+      // inverse rotation: x1' = x1 cos + x2 sin, x2' = x2 cos - x1 sin
+      out[e] = d < HALF ? (v[e] * cs + pv[e] * sn) * scale : (v[e] * cs - pv[e] * sn) * scale;
+    }
+  }
+  if constexpr (E == 4) *(u32x2*)(row + d0) = u32x2{pack_bf2(out[0], out[1]), pack_bf2(out[2], out[3])};
+  else *(uint32_t*)(row + d0) = pack_bf2(out[0], out[1]);
 }
 
 // dQ for 128 queries of one head (4 waves x 32 queries): loops over the key
@@ -646,6 +723,22 @@ hipError_t attn_fwd_t(const AttnShape& sh, const bf16_t* qkv, bf16_t* o, float* 
   return hipGetLastError();
 }
 
+// Split of each kv head's query-head group over workgroups of the dK/dV
+// kernel: the smallest divisor of the group size that gives at least two
+// workgroups per compute unit (256 CUs), or the whole group.
+int dkdv_split(const AttnShape& sh) {
+  const int G = sh.nq / sh.nkv;
+  const int64_t g1 = (int64_t)((sh.seq + BWD_BKV - 1) / BWD_BKV) * sh.nkv * sh.batch;
+  for (int h = 1; h < G; ++h)
+    if (G % h == 0 && g1 * h >= 512) return h;
+  return G;
+}
+
+// Bytes of the backward workspace before the partial sums: D, then the base-2 log-sum-exp.
+int64_t bwd_ws_head(const AttnShape& sh) {
+  return 2 * (int64_t)sh.batch * sh.seq * sh.nq * (int64_t)sizeof(float);
+}
+
 template <int D>
 hipError_t attn_bwd_t(const AttnShape& sh, const bf16_t* qkv, const bf16_t* o, const float* lse, const bf16_t* dout,
                       bf16_t* dqkv, const float* rope_cs, void* ws, hipStream_t s) {
@@ -657,12 +750,24 @@ hipError_t attn_bwd_t(const AttnShape& sh, const bf16_t* qkv, const bf16_t* o, c
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const float scale = 1.0f / sqrtf((float)(sh.d_scale > 0 ? sh.d_scale : D));
-  const unsigned gkv = (unsigned)((sh.seq + BWD_BKV - 1) / BWD_BKV) * sh.nkv * sh.batch;
-  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D>), dim3(gkv), dim3(256), 0, s, sh, qkv, dout, (const float*)lse2,
-                     (const float*)Dv,
-                     dqkv, rope_cs, scale, scale * LOG2E);
+  const int hsplit = dkdv_split(sh);
+  float* part = hsplit > 1 ? (float*)((char*)ws + bwd_ws_head(sh)) : nullptr;
+  const unsigned gkv = (unsigned)((sh.seq + BWD_BKV - 1) / BWD_BKV) * sh.nkv * sh.batch * hsplit;
+  if (part)
+    hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, true>), dim3(gkv), dim3(256), 0, s, sh, qkv, dout, (const float*)lse2,
+                       (const float*)Dv, dqkv, rope_cs, scale, scale * LOG2E, hsplit, part);
+  else
+    hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, false>), dim3(gkv), dim3(256), 0, s, sh, qkv, dout,
+                       (const float*)lse2, (const float*)Dv, dqkv, rope_cs, scale, scale * LOG2E, 1, nullptr);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (part) {
+    const int64_t rows = T * sh.nkv;  // one wave each, four per workgroup
+    hipLaunchKernelGGL((attn_bwd_dkdv_reduce<D>), dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, sh, hsplit,
+                       (const float*)part, dqkv, rope_cs, scale);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   const unsigned gq = (unsigned)((sh.seq + BQ - 1) / BQ) * sh.nq * sh.batch;
   hipLaunchKernelGGL((attn_bwd_dq_kernel<D>), dim3(gq), dim3(256), 0, s, sh, qkv, dout, (const float*)lse2,
                      (const float*)Dv, dqkv, rope_cs, scale, scale * LOG2E);
@@ -678,8 +783,11 @@ hipError_t attn_fwd(const AttnShape& sh, const bf16_t* qkv, bf16_t* o, float* ls
 }
 
 size_t attn_bwd_workspace(const AttnShape& sh) {
-  const int64_t T = (int64_t)sh.batch * sh.seq;
-  return 2 * (size_t)(T * sh.nq) * sizeof(float);  // D, then the base-2 log-sum-exp
+  // D and the base-2 log-sum-exp of every query, then (when the dK/dV group
+  // is split) the fp32 partial dK | dV rows of every split
+  const int hsplit = dkdv_split(sh);
+  const int64_t part = hsplit > 1 ? (int64_t)hsplit * sh.batch * sh.seq * sh.nkv * 2 * sh.d * (int64_t)sizeof(float) : 0;
+  return (size_t)(bwd_ws_head(sh) + part);
 }
 
 hipError_t attn_bwd(const AttnShape& sh, const bf16_t* qkv, const bf16_t* o, const float* lse, const bf16_t* dout,
