@@ -136,15 +136,24 @@ def test_attention_core(name, B, S, nq, nkv, d, std):
     assert fro_rel(g[:, Dq:Dq + Dkv], dk.reshape(T, Dkv)) < GRAD_TOL
 
 
-def test_attention_core_8k_sampled_group():
-    """Attention at the long-context shape (1 x 8192, 24 query heads / 8 kv
-    heads x 128) in its full launch configuration; the oracle computes one kv
-    group (kv head 5 and its query heads 15..17) over all 8192 positions."""
+SAMPLED_GROUP_CASES = [
+    # name, batch, seq, nq, nkv, d, kv head checked.  The dK/dV kernel splits a
+    # kv head's query-head group over workgroups when (seq/128) * nkv * batch
+    # is below 512: "8k" fills the chip unsplit (512 workgroups); "split2of4"
+    # (256 workgroups, groups of 4) sums two partials of two heads each.
+    ("8k", 1, 8192, 24, 8, 128, 5),
+    ("split2of4", 1, 2048, 64, 16, 64, 11),
+]
+
+
+@pytest.mark.parametrize("name,B,S,nq,nkv,d,kvh", SAMPLED_GROUP_CASES, ids=[c[0] for c in SAMPLED_GROUP_CASES])
+def test_attention_core_sampled_group(name, B, S, nq, nkv, d, kvh):
+    """Attention at a long or many-head shape in its full launch
+    configuration; the oracle computes one kv group (kv head kvh and its query
+    heads) over all positions."""
     need_gpu()
-    B, S, nq, nkv, d = 1, 8192, 24, 8, 128
     G = nq // nkv
-    kvh = 5
-    say("attention core 8k, kv group 5")
+    say(f"attention core {name}, kv group {kvh}")
     c = configs.TINY.with_(batch=B, seq=S, n_q_heads=nq, n_kv_heads=nkv, head_dim=d, hidden=nq * d)
     T, Dq, Dkv = B * S, nq * d, nkv * d
     q = bf16_randn((T, Dq), 21)
