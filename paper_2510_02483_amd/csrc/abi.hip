@@ -5,7 +5,9 @@
 #include <string.h>
 
 #include <algorithm>
+#include <array>
 #include <atomic>
+#include <initializer_list>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -211,8 +213,17 @@ ls::AttnShape attn_shape(const Dims& m) {
   return ls::AttnShape{(int)m.B, (int)m.S, (int)m.nq, (int)m.nkv, (int)m.dp, (int)m.d};
 }
 
+// fp32 partial sums of the weight-gradient products that split K (their
+// output tiles alone would leave most compute units idle)
+int64_t kpart_floats(std::initializer_list<std::array<int64_t, 3>> shapes) {
+  int64_t n = 0;
+  for (const auto& mnk : shapes) n = std::max(n, ls::gemm_kpart_floats((int)mnk[0], (int)mnk[1], (int)mnk[2]));
+  return n;
+}
+
 struct AttnWs {
-  size_t rope, dO, dqkv, dh1, partial, core, wpad, wopad, gpad, gopad, total;
+  size_t rope, dO, dqkv, dh1, partial, core, wpad, wopad, gpad, gopad, kpart, total;
+  int64_t kpart_floats;
 };
 AttnWs attn_ws_layout(const Dims& m) {
   Carver c;
@@ -228,12 +239,15 @@ AttnWs attn_ws_layout(const Dims& m) {
   w.dh1 = c.take(m.T * m.H * 2);
   w.partial = c.take(norm_partial_bytes(m));
   w.core = c.take(ls::attn_bwd_workspace(attn_shape(m)));
+  w.kpart_floats = kpart_floats({{m.H, m.Pq, m.T}, {m.Pqkv, m.H, m.T}});  // dWo, dWqkv
+  w.kpart = c.take((size_t)w.kpart_floats * 4);
   w.total = c.off;
   return w;
 }
 
 struct MlpWs {
-  size_t dgu, dh2, partial, total;
+  size_t dgu, dh2, partial, kpart, total;
+  int64_t kpart_floats;
 };
 MlpWs mlp_ws_layout(const Dims& m) {
   Carver c;
@@ -241,6 +255,8 @@ MlpWs mlp_ws_layout(const Dims& m) {
   w.dgu = c.take(m.T * 2 * m.I * 2);
   w.dh2 = c.take(m.T * m.H * 2);
   w.partial = c.take(norm_partial_bytes(m));
+  w.kpart_floats = kpart_floats({{m.H, m.I, m.T}, {2 * m.I, m.H, m.T}});  // dWd, dWg/dWu
+  w.kpart = c.take((size_t)w.kpart_floats * 4);
   w.total = c.off;
   return w;
 }
@@ -428,6 +444,8 @@ int run_attn_bwd(const ls_block_cfg& cfg, const Dims& m, const bf16_t* x, const 
     g.F[0] = m.pad ? at<float>(ws, wl.gopad) : gr->wo;
     g.ldf = m.Pq;
     g.accumulate = m.pad ? 0 : accumulate;
+    g.kpart = at<float>(ws, wl.kpart);
+    g.kpart_floats = wl.kpart_floats;
     LS_STEP("dWo", st, ls::gemm(g, st));
     if (m.pad)
       LS_STEP("dWo", st, ls::unpad_head_cols(at<float>(ws, wl.gopad), gr->wo, (int)m.H, (int)m.nq, (int)m.d,
@@ -477,6 +495,8 @@ int run_attn_bwd(const ls_block_cfg& cfg, const Dims& m, const bf16_t* x, const 
       g.accumulate = accumulate;
     }
     g.ldf = m.H;
+    g.kpart = at<float>(ws, wl.kpart);
+    g.kpart_floats = wl.kpart_floats;
     LS_STEP("dWqkv", st, ls::gemm(g, st));
     if (m.pad) {
       const float* gp = at<float>(ws, wl.gpad);
@@ -587,6 +607,8 @@ int run_mlp_bwd(const ls_block_cfg& cfg, const Dims& m, const bf16_t* x2, const 
     g.F[0] = gr->wd;
     g.ldf = m.I;
     g.accumulate = accumulate;
+    g.kpart = at<float>(ws, wl.kpart);
+    g.kpart_floats = wl.kpart_floats;
     LS_STEP("dWd", st, ls::gemm(g, st));
   }
   {  // dh2 = dg Wg + du Wu
@@ -623,6 +645,8 @@ int run_mlp_bwd(const ls_block_cfg& cfg, const Dims& m, const bf16_t* x2, const 
     g.f_start[1] = (int)m.I;
     g.ldf = m.H;
     g.accumulate = accumulate;
+    g.kpart = at<float>(ws, wl.kpart);
+    g.kpart_floats = wl.kpart_floats;
     LS_STEP("dWg/dWu", st, ls::gemm(g, st));
   }
   LS_STEP("rmsnorm bwd", st,

@@ -37,6 +37,7 @@
 // its second, so that a lane ends up holding four consecutive output columns
 // of one row: 8-byte bf16 / 16-byte fp32 stores, and the RoPE and SwiGLU
 // partners of a column sit in the same lane.
+#include <algorithm>
 #include <atomic>
 #include <type_traits>
 
@@ -277,8 +278,11 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = wave / 2, wn = wave % 2;
   const int tiles_m = (p.M + BM - 1) / BM, tiles_n = (p.N + BN - 1) / BN;
+  // fp32 weight gradients may split K: workgroup x runs slice x / tiles of tile x % tiles
+  const int ks = EPI == EPI_F32 ? p.ksplit : 1;
+  const int slice = ks > 1 ? (int)blockIdx.x / (tiles_m * tiles_n) : 0;
   int tm, tn;
-  map_tile(blockIdx.x, tiles_m, tiles_n, tm, tn);
+  map_tile((int)blockIdx.x - slice * tiles_m * tiles_n, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
   const int K = p.K;
 
@@ -290,8 +294,17 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
     S1 = min(p.b_start[1], K);
     S2 = max(S1, min(p.b_start[2], K));
   }
-  auto seg_end = [&](int k) { return k < S1 ? S1 : (k < S2 ? S2 : K); };
-  const int nk = (S1 + KT - 1) / KT + (S2 - S1 + KT - 1) / KT + (K - S2 + KT - 1) / KT;
+  int kbeg = 0, kend = K;  // k range of this workgroup (a slice of the k tiles when K is split)
+  auto seg_end = [&](int k) { return min(kend, k < S1 ? S1 : (k < S2 ? S2 : K)); };
+  int nk = (S1 + KT - 1) / KT + (S2 - S1 + KT - 1) / KT + (K - S2 + KT - 1) / KT;
+  if (ks > 1) {  // slice j: k tiles [j nk / ks, (j+1) nk / ks) of the whole sequence
+    const int n0t = (S1 + KT - 1) / KT, n1t = (S2 - S1 + KT - 1) / KT;
+    auto k_of = [&](int t) { return t < n0t ? t * KT : (t < n0t + n1t ? S1 + (t - n0t) * KT : S2 + (t - n0t - n1t) * KT); };
+    const int t0 = (int)((int64_t)slice * nk / ks), t1 = (int)((int64_t)(slice + 1) * nk / ks);
+    kbeg = k_of(t0);
+    kend = t1 == nk ? K : k_of(t1);
+    nk = t1 - t0;
+  }
 
   OpLoads<NA> la;
   OpLoads<NB> lb;
@@ -424,7 +437,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
     for (int q = 0; q < NL; ++q) n += BAR_AT + (q * LSPAN) / NL + BS * NMF < KSTEPS * NMF;
     return n;
   }();
-  set_cursor(0);
+  set_cursor(kbeg);
 #pragma unroll
   for (int q = 0; q < NL; ++q) issue(q, 0);
   set_cursor(ck + kval);
@@ -479,14 +492,16 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
 
   if constexpr (EPI == EPI_F32) {
     // fp32 weight gradients straight from the registers: a lane's 4 columns are
-    // 16 contiguous bytes (read-modify-write with accumulate)
+    // 16 contiguous bytes (read-modify-write with accumulate).  Slices 1.. of a
+    // split K store plain partial sums ([M][N] each) for kpart_reduce_kernel.
+    float* kp = slice > 0 ? p.kpart + (int64_t)(slice - 1) * p.M * p.N : nullptr;
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
       const int m = mw + 32 * i + lr;
       const int sg = m >= p.f_start[2] ? 2 : (m >= p.f_start[1] ? 1 : 0);
       float* base = sg == 2 ? p.F[2] : (sg == 1 ? p.F[1] : p.F[0]);
       const int fs = sg == 2 ? p.f_start[2] : (sg == 1 ? p.f_start[1] : 0);
-      float* row = base + (int64_t)(m - fs) * p.ldf;
+      float* row = kp ? kp + (int64_t)m * p.N : base + (int64_t)(m - fs) * p.ldf;
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
 #pragma unroll
@@ -494,7 +509,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
           const int n = nw + 32 * j + 8 * q + 4 * lh;
           f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
           if (m < p.M && n < p.N) {
-            if (p.accumulate) v += *(const f32x4*)(row + n);
+            if (p.accumulate && !kp) v += *(const f32x4*)(row + n);
             *(f32x4*)(row + n) = v;
           }
         }
@@ -698,8 +713,25 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
 template <bool AK, bool BKC, int EPI, int BM, int BN>
 hipError_t launch(const GemmArgs& a, hipStream_t s) {
   const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_kernel<AK, BKC, EPI, BM, BN>), dim3(tiles), dim3(NT), 0, s, a);
+  hipLaunchKernelGGL((gemm_kernel<AK, BKC, EPI, BM, BN>), dim3(tiles * a.ksplit), dim3(NT), 0, s, a);
   return hipGetLastError();
+}
+
+// F (already holding slice 0's result, with the accumulate read) += the
+// partial sums of slices 1 .. ksplit-1, added in slice order.  N % 4 == 0.
+__global__ __launch_bounds__(256) void kpart_reduce_kernel(GemmArgs p) {
+  const int64_t per = (int64_t)p.M * p.N, n4 = per / 4;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256) {
+    const int64_t e = 4 * i;
+    const int m = (int)(e / p.N), n = (int)(e - (int64_t)m * p.N);
+    const int sg = m >= p.f_start[2] ? 2 : (m >= p.f_start[1] ? 1 : 0);
+    float* base = sg == 2 ? p.F[2] : (sg == 1 ? p.F[1] : p.F[0]);
+    const int fs = sg == 2 ? p.f_start[2] : (sg == 1 ? p.f_start[1] : 0);
+    float* dst = base + (int64_t)(m - fs) * p.ldf + n;
+    f32x4 v = *(const f32x4*)dst;
+    for (int j = 0; j < p.ksplit - 1; ++j) v += *(const f32x4*)(p.kpart + j * per + e);
+    *(f32x4*)dst = v;
+  }
 }
 
 int compute_units() {
@@ -714,6 +746,17 @@ int compute_units() {
 }
 
 std::atomic<int> g_tile_override{0};  // 0: automatic, else 1000 * BM + BN
+
+// Slices of K for an fp32 weight-gradient product whose 256 x 256 tiles fill
+// at most half the compute units: as many as fill them, at most 8, each at
+// least 8 k tiles deep.
+int ksplit_of(int M, int N, int K) {
+  const int64_t tiles = (int64_t)((M + 255) / 256) * ((N + 255) / 256);
+  const int ncu = compute_units();
+  if (N % 4 != 0 || tiles == 0 || 2 * tiles > ncu) return 1;
+  const int64_t s = std::min<int64_t>(std::min<int64_t>(ncu / tiles, ((int64_t)K + KT - 1) / KT / 8), 8);
+  return s < 2 ? 1 : (int)s;
+}
 
 // Tile shape (1000 * BM + BN) of a launch: among the shapes the kernel variant
 // allows, the one with the fewest waves of workgroups times tile area; a
@@ -754,7 +797,14 @@ int gemm_tile_override(int bm, int bn) {
   return 0;
 }
 
-hipError_t gemm(const GemmArgs& a, hipStream_t s) {
+int64_t gemm_kpart_floats(int M, int N, int K) {
+  const int ks = ksplit_of(M, N, K);
+  return ks > 1 ? (int64_t)(ks - 1) * M * N : 0;
+}
+
+hipError_t gemm(const GemmArgs& args, hipStream_t s) {
+  GemmArgs a = args;
+  a.ksplit = 1;
   // A k-contiguous B split over buffers (or gate/up interleaved) is loaded a
   // wave's 64 rows at a time from one buffer: segments start at multiples of 64.
   if (a.b_kcontig && ((a.b_start[1] % 64 && a.b_start[1] < a.N) || (a.b_start[2] % 64 && a.b_start[2] < a.N)))
@@ -783,6 +833,18 @@ hipError_t gemm(const GemmArgs& a, hipStream_t s) {
     }
   } else if (!a.a_kcontig && !a.b_kcontig) {
     if (a.epi == EPI_F32) {
+      int ks = ksplit_of(a.M, a.N, a.K);
+      if (ks > 1)  // as many slices as the workspace holds
+        ks = (int)std::min<int64_t>(ks, a.kpart ? a.kpart_floats / ((int64_t)a.M * a.N) + 1 : 1);
+      if (ks > 1) {
+        a.ksplit = ks;
+        hipError_t e = launch<false, false, EPI_F32, 256, 256>(a, s);
+        if (e != hipSuccess) return e;
+        const int64_t n4 = (int64_t)a.M * a.N / 4;
+        const unsigned grid = (unsigned)std::min<int64_t>((n4 + 255) / 256, 256 * 8);
+        hipLaunchKernelGGL(kpart_reduce_kernel, dim3(grid), dim3(256), 0, s, a);
+        return hipGetLastError();
+      }
       switch (pick_tile(a.M, a.N, true, true)) {
         case 192192: return launch<false, false, EPI_F32, 192, 192>(a, s);
         case 192256: return launch<false, false, EPI_F32, 192, 256>(a, s);

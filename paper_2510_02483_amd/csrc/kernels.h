@@ -51,9 +51,18 @@ struct GemmArgs {
   int f_start[3] = {0, 1 << 30, 1 << 30};
   int64_t ldf = 0;
   int accumulate = 0;
+  // EPI_F32: fp32 workspace for splitting K over workgroups when the output
+  // tiles fill at most half the compute units ((slices - 1) * M * N floats,
+  // see gemm_kpart_floats); null or smaller means fewer slices or none.
+  float* kpart = nullptr;
+  int64_t kpart_floats = 0;
+  int ksplit = 1;  // slices of K (set by gemm())
 };
 
 hipError_t gemm(const GemmArgs& a, hipStream_t s);
+// Floats of GemmArgs::kpart with which an EPI_F32 product of this shape runs
+// with its full split of K (0: it is not split).
+int64_t gemm_kpart_floats(int M, int N, int K);
 // Force the tile shape of later gemm launches (bm, bn in {256, 192}; 0, 0 =
 // automatic).  Variants that only exist as 256 x 256 ignore it.  -1 on bad sizes.
 int gemm_tile_override(int bm, int bn);

@@ -30,6 +30,10 @@ ONE_TOKEN = configs.BlockConfig("one-token", 16, batch=3, seq=1, hidden=256, n_q
                                 intermediate=688, rope_theta=1e4)
 D72 = configs.BlockConfig("d72", 15, batch=2, seq=96, hidden=288, n_q_heads=4, n_kv_heads=1, head_dim=72,
                           intermediate=392, rope_theta=5e5)
+# many tokens, small weights: each weight-gradient product has 1-6 output tiles
+# and splits its 3000-deep contraction over 5 workgroups (the last slice ragged)
+LONG_NARROW = configs.BlockConfig("long-narrow", 18, batch=2, seq=1500, hidden=256, n_q_heads=4, n_kv_heads=2,
+                                  head_dim=64, intermediate=688, rope_theta=1e4)
 
 BLOCK_CASES = [
     ("d104-gqa", D104_GQA, {"gamma": "random"}),
@@ -42,6 +46,7 @@ BLOCK_CASES = [
     ("mid-d64", MID_D64, {"gamma": "random"}),
     ("mid-d128", MID_D128, {}),
     ("mha-d128-sharp", MHA_D128, {"wq_std": 0.3}),
+    ("long-narrow", LONG_NARROW, {"gamma": "random"}),
 ]
 
 
@@ -79,7 +84,7 @@ def test_block_parity(name, c, kw):
     compare_block(c, blk, fwd, gr)
 
 
-@pytest.mark.parametrize("c", [MID_D64, D104_GQA], ids=["d64", "d104-padded"])
+@pytest.mark.parametrize("c", [MID_D64, D104_GQA, LONG_NARROW], ids=["d64", "d104-padded", "split-k"])
 def test_sublayers_match_block_call(c):
     """ls_attn_fwd / ls_mlp_fwd / ls_mlp_bwd / ls_attn_bwd chained by hand give
     the oracle's intermediates (x2, dx2) and final results (also with heads of
@@ -116,11 +121,13 @@ def test_sublayers_match_block_call(c):
         assert fro_rel(f64(g[n]), gr[n]) < GRAD_TOL, n
 
 
-def test_accumulate_and_side_stream():
-    """accumulate=1 adds into the fp32 gradients; a non-default stream works."""
+@pytest.mark.parametrize("c", [configs.TINY, LONG_NARROW], ids=["tiny", "split-k"])
+def test_accumulate_and_side_stream(c):
+    """accumulate=1 adds into the fp32 gradients (also where the weight
+    gradients split K: the first slice adds, the others' partial sums follow);
+    a non-default stream works."""
     need_gpu()
-    c = configs.TINY
-    say("accumulate / side stream")
+    say(f"accumulate / side stream {c.name}")
     host = inputs.make_inputs(c, gamma="random")
     blk = L.Block(c, host)
     s = torch.cuda.Stream()
