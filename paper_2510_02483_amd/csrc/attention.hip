@@ -440,11 +440,14 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnShape sh, con
   // offset plus an instruction offset.
   auto tile = [&](int t, int st, int st1, int st2) {
     const int q0 = q_begin + (t % nqt) * BWD_BQ;
-    // causal mask: element r of block qb is query q0 + 4lh + c with
-    // c = 32qb + 8(r/4) + r%4, kept when c >= lo, i.e. q >= kvrow.  Queries
-    // past the end of the sequence need no mask: their Q, dO, LSE and D read
-    // as zero, so they add nothing to dK or dV.
+    // causal mask, on the tiles at the diagonal only (some query of the tile
+    // precedes some key of the wave): element r of block qb is query
+    // q0 + 4lh + c with c = 32qb + 8(r/4) + r%4, kept when c >= lo, i.e.
+    // q >= kvrow; a masked score becomes -inf, so its probability is
+    // exp2(-inf) = 0.  Queries past the end of the sequence need no mask: their
+    // Q, dO, LSE and D read as zero, so they add nothing to dK or dV.
     const int lo = kvrow - q0 - 4 * lh;
+    const bool diag = q0 < kv0 + 32 * wave + 31;
     static_for<NSLOT>([&](auto j_c) {
       constexpr int j = decltype(j_c)::value;
       constexpr int qb = j / NB, k = j % NB;
@@ -463,14 +466,20 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnShape sh, con
       } else if constexpr (k < P1 + P2) {  // dP = dO V^T, meanwhile P = exp2(S sl2 - LSE2)
         constexpr int c = k - P1, PER = 16 / P2;
         pacc = mfma32(a, vf[c], c == 0 ? f32x16{} : pacc);
+        if constexpr (c == 0) {
+          if (diag) {
+            asm volatile("");  // keeps the block a branch rather than selects on every tile
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+              if (32 * qb + 8 * (r >> 2) + (r & 3) < lo) sacc[r] = -INFINITY;
+          }
+        }
         static_for<PER>([&](auto u_c) {
           constexpr int r = c * PER + decltype(u_c)::value, rq = r >> 2, e = r & 3;
           // the next group's log-sum-exp, one group ahead
           if constexpr (e == 0 && rq < 3) Lq[(rq + 1) & 1] = *(const f32x4*)&stg[st].l[32 * qb + 8 * (rq + 1) + 4 * lh];
           if constexpr (r == 12) Dq[0] = *(const f32x4*)&stg[st].d[32 * qb + 4 * lh];
-          float p = ex2(fmaf(sacc[r], sl2, -Lq[rq & 1][e]));
-          if (32 * qb + 8 * rq + e < lo) p = 0.f;
-          sacc[r] = p;
+          sacc[r] = ex2(fmaf(sacc[r], sl2, -Lq[rq & 1][e]));
           if constexpr ((r & 7) == 7) pf[r >> 3] = pack_frag(sacc, r - 7);
         });
       } else if constexpr (k < P1 + P2 + P3) {  // dV^T += dO^T P, meanwhile dS = P (dP - D)
