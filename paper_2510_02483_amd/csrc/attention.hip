@@ -184,9 +184,53 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnShape sh, const bf
     for (int r = 0; r < 16; ++r) oacc[i][r] = 0.f;
   float m = -INFINITY, l = 0.f;
 
+  // LDS byte addresses of this lane's operand reads, computed once and held
+  // in registers (opaque to the compiler, which would otherwise recompute the
+  // swizzled offsets for every read): the K rows of each 16-wide d step, and
+  // the V columns of each 32-wide d block and row group.  The stage, the
+  // 32-key block and the 16-key step only add constants.
+  constexpr int NSD = D / 16, NDB = D / 32;
+  uint32_t ka[NSD], va[NDB][2];
+  {
+    const uint32_t kb = lds_offset(&Ks[0][0]), vb = lds_offset(&Vs[0][0]);
+#pragma unroll
+    for (int s = 0; s < NSD; ++s) {
+      ka[s] = kb + 2u * (uint32_t)(lr * D + 8 * ((2 * s + lh) ^ tile_swz<D>(lr)));
+      asm volatile("" : "+v"(ka[s]));
+    }
+    const int g = lane >> 4, q = lane & 15;
+#pragma unroll
+    for (int i = 0; i < NDB; ++i)
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const int kk = 4 * (g >> 1) + 8 * hh + (q >> 2), col = 32 * i + 16 * (g & 1) + 4 * (q & 3);
+        va[i][hh] = vb + 2u * (uint32_t)(kk * D + 8 * ((col >> 3) ^ tile_swz<D>(kk)) + (col & 7));
+        asm volatile("" : "+v"(va[i][hh]));
+      }
+  }
+  constexpr uint32_t STAGE = BKV * D * 2;
+  // K fragment (as row_frag) of key block bb, d step s, stage ST
+  auto kfrag = [&](auto st_c, int bb, int s) -> u32x4 {
+    return *(const LDS_AS u32x4*)(size_t)(ka[s] + (uint32_t)(decltype(st_c)::value * STAGE + bb * 32 * D * 2));
+  };
+  // V^T fragment (as colt_frag) of d block i, key step s, stage ST
+  auto vfrag = [&](auto st_c, int i, int s) -> u32x4 {
+    u32x4 out;
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      const uint32_t a = va[i][hh] + (uint32_t)(decltype(st_c)::value * STAGE + s * 16 * D * 2);
+      const u32x2 w = __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS s16x4*)(size_t)a));
+      out[2 * hh] = w[0];
+      out[2 * hh + 1] = w[1];
+    }
+    return out;
+  };
+
   sync_lds();
-  for (int kt = 0; kt < nkt; ++kt) {
-    const int cur = kt & 1, kv0 = kt * BKV;
+  // one 64-key tile in stage CUR (a constant: the loop below runs two per pass)
+  auto step = [&](auto cur_c, int kt) {
+    constexpr int cur = decltype(cur_c)::value;
+    const int kv0 = kt * BKV;
     if (kt + 1 < nkt) {
       load_tile<D, BKV>(rs, ld, kv0 + BKV, S, kcol, Ks[cur ^ 1], wave, lane);
       load_tile<D, BKV>(rs, ld, kv0 + BKV, S, vcol, Vs[cur ^ 1], wave, lane);
@@ -201,7 +245,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnShape sh, const bf
       for (int s = 0; s < D / 16; ++s)
 #pragma unroll
         for (int bb = 0; bb < BKV / 32; ++bb)
-          sacc[bb] = mfma32(row_frag<D>(Ks[cur], 32 * bb + lr, s, lh), qf[s], sacc[bb]);
+          sacc[bb] = mfma32(kfrag(cur_c, bb, s), qf[s], sacc[bb]);
       // lane holds query qrow, keys kv0 + 32bb + 8(r/4) + 4lh + r%4
       if (kv0 + BKV - 1 > wave_qmin) {
 #pragma unroll
@@ -238,10 +282,14 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnShape sh, const bf
       for (int s = 0; s < BKV / 16; ++s) {
         const u32x4 pf = pack_frag(sacc[s >> 1], 8 * (s & 1));
 #pragma unroll
-        for (int i = 0; i < D / 32; ++i) oacc[i] = mfma32(colt_frag<D>(Vs[cur], 32 * i, s, lane), pf, oacc[i]);
+        for (int i = 0; i < D / 32; ++i) oacc[i] = mfma32(vfrag(cur_c, i, s), pf, oacc[i]);
       }
     }
     sync_lds();
+  };
+  for (int kt = 0; kt < nkt; kt += 2) {
+    step(std::integral_constant<int, 0>{}, kt);
+    if (kt + 1 < nkt) step(std::integral_constant<int, 1>{}, kt + 1);
   }
 
   if (qrow < S) {
