@@ -703,15 +703,51 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(AttnShape sh, const
 #pragma unroll
     for (int r = 0; r < 16; ++r) dq[i][r] = 0.f;
 
-  // MFMA A operand of slot j of the tile in stage st.
-  auto operand = [&](auto j_c, int st) -> u32x4 {
-    constexpr int j = decltype(j_c)::value;
-    if constexpr (j < 2 * PS) {
+  // LDS byte addresses of this lane's operand reads, computed once and held
+  // in registers the compiler cannot rematerialise: K and V rows (one layout)
+  // for each 16-wide d step, and K^T columns for each 32-wide d block and row
+  // group.  The tile's stage, the array, the 32-key block and the 16-key step
+  // only add constants.
+  uint32_t ra[NSD], ta[NI][2];
+  {
+    const uint32_t kb = lds_offset(&Ks[0][0]);
+#pragma unroll
+    for (int s = 0; s < NSD; ++s) {
+      ra[s] = kb + 2u * (uint32_t)(lr * D + 8 * ((2 * s + lh) ^ tile_swz<D>(lr)));
+      asm volatile("" : "+v"(ra[s]));
+    }
+    const int g = lane >> 4, q = lane & 15;
+#pragma unroll
+    for (int i = 0; i < NI; ++i)
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const int kk = 4 * (g >> 1) + 8 * hh + (q >> 2), col = 32 * i + 16 * (g & 1) + 4 * (q & 3);
+        ta[i][hh] = kb + 2u * (uint32_t)(kk * D + 8 * ((col >> 3) ^ tile_swz<D>(kk)) + (col & 7));
+        asm volatile("" : "+v"(ta[i][hh]));
+      }
+  }
+  constexpr uint32_t STAGE = BKV * D * 2;
+  const uint32_t v_minus_k = lds_offset(&Vs[0][0]) - lds_offset(&Ks[0][0]);
+
+  // MFMA A operand of slot j of the tile in stage ST.
+  auto operand = [&](auto j_c, auto st_c) -> u32x4 {
+    constexpr int j = decltype(j_c)::value, st = decltype(st_c)::value;
+    if constexpr (j < 2 * PS) {  // row_frag of K (k even) or V (k odd)
       constexpr int bb = j / PS, k = j % PS;
-      return row_frag<D>((k & 1) ? Vs[st] : Ks[st], 32 * bb + lr, k >> 1, lh);
-    } else {
+      const uint32_t a = ra[k >> 1] + (uint32_t)(st * STAGE + bb * 32 * D * 2) + ((k & 1) ? v_minus_k : 0u);
+      return *(const LDS_AS u32x4*)(size_t)a;
+    } else {  // colt_frag of K
       constexpr int bb = (j - 2 * PS) / PQ, c = (j - 2 * PS) % PQ;
-      return colt_frag<D>(Ks[st], 32 * (c % NI), 2 * bb + c / NI, lane);
+      constexpr int i = c % NI, s = 2 * bb + c / NI;
+      u32x4 out;
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const uint32_t a = ta[i][hh] + (uint32_t)(st * STAGE + s * 16 * D * 2);
+        const u32x2 w = __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS s16x4*)(size_t)a));
+        out[2 * hh] = w[0];
+        out[2 * hh + 1] = w[1];
+      }
+      return out;
     }
   };
 
@@ -731,14 +767,16 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(AttnShape sh, const
   };
 
   sync_lds();
-  for (int kt = 0; kt < nkt; ++kt) {
-    const int cur = kt & 1, kv0 = kt * BKV;
+  // one 64-key tile in stage CUR (a constant: the loop below runs two per pass)
+  auto step = [&](auto cur_c, int kt) {
+    constexpr int cur = decltype(cur_c)::value;
+    const int kv0 = kt * BKV;
     if (kt + 1 < nkt) {
       load_tile<D, BKV, true>(rs, ld, kv0 + BKV, S, kcol, Ks[cur ^ 1], wave, lane);
       load_tile<D, BKV, true>(rs, ld, kv0 + BKV, S, vcol, Vs[cur ^ 1], wave, lane);
     }
     const int hi = qrow - kv0 - 4 * lh;
-    static_for<RA>([&](auto j_c) { ring[decltype(j_c)::value] = operand(j_c, cur); });
+    static_for<RA>([&](auto j_c) { ring[decltype(j_c)::value] = operand(j_c, cur_c); });
     static_for<NSLOT>([&](auto j_c) {
       constexpr int j = decltype(j_c)::value;
       __builtin_amdgcn_sched_barrier(0);
@@ -763,10 +801,14 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(AttnShape sh, const
           });
         }
       }
-      if constexpr (j + RA < NSLOT) ring[(j + RA) % RING] = operand(std::integral_constant<int, j + RA>{}, cur);
+      if constexpr (j + RA < NSLOT) ring[(j + RA) % RING] = operand(std::integral_constant<int, j + RA>{}, cur_c);
       __builtin_amdgcn_sched_barrier(0);
     });
     sync_lds();
+  };
+  for (int kt = 0; kt < nkt; kt += 2) {
+    step(std::integral_constant<int, 0>{}, kt);
+    if (kt + 1 < nkt) step(std::integral_constant<int, 1>{}, kt + 1);
   }
   if (!qok) return;
   unrotate_store<D>(dq, scale, rope_cs, S, qrow, lh, dqkv + ((int64_t)b * S + qrow) * ld + h * D);
