@@ -137,6 +137,49 @@ LS_DEV u32x4 colt_frag(const bf16_t* t, int c32, int s, int lane) {
   return out;
 }
 
+// The same two kinds of operand reads by LDS byte address: this lane's
+// addresses relative to a tile at `base` take only D/16 values for row reads
+// (row lr, d step s; the 32-row block adds a constant) and 2·D/32 for
+// transposing reads (d block i, row group hh; the 16-row step adds a
+// constant), so they are computed once and held in registers the compiler
+// cannot rematerialise.  With the other tiles in the same layout at constant
+// distances (stages, arrays), every read is then one LDS instruction with an
+// immediate offset.
+template <int D>
+struct FragAddr {
+  uint32_t row[D / 16], col[D / 32][2];
+  LS_DEV FragAddr(uint32_t base, int lane) {
+    const int lr = lane & 31, lh = lane >> 5, g = lane >> 4, q = lane & 15;
+#pragma unroll
+    for (int s = 0; s < D / 16; ++s) {
+      row[s] = base + 2u * (uint32_t)(lr * D + 8 * ((2 * s + lh) ^ tile_swz<D>(lr)));
+      asm volatile("" : "+v"(row[s]));
+    }
+#pragma unroll
+    for (int i = 0; i < D / 32; ++i)
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const int kk = 4 * (g >> 1) + 8 * hh + (q >> 2), c = 32 * i + 16 * (g & 1) + 4 * (q & 3);
+        col[i][hh] = base + 2u * (uint32_t)(kk * D + 8 * ((c >> 3) ^ tile_swz<D>(kk)) + (c & 7));
+        asm volatile("" : "+v"(col[i][hh]));
+      }
+  }
+  // row_frag(tile at base + off, 32-row block, s, lh) for off = block * 32 * D * 2 + ...
+  LS_DEV u32x4 rows(int s, uint32_t off) const { return *(const LDS_AS u32x4*)(size_t)(row[s] + off); }
+  // colt_frag(tile at base + off, 32 i, step, lane) for off = step * 16 * D * 2 + ...
+  LS_DEV u32x4 cols(int i, uint32_t off) const {
+    u32x4 out;
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      const u32x2 w = __builtin_bit_cast(
+          u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS s16x4*)(size_t)(col[i][hh] + off)));
+      out[2 * hh] = w[0];
+      out[2 * hh + 1] = w[1];
+    }
+    return out;
+  }
+};
+
 // Query-tile workgroups (forward, dQ): the 1-D grid runs the longest tiles
 // (highest query index, most keys) first.
 struct QTile {
@@ -184,47 +227,11 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnShape sh, const bf
     for (int r = 0; r < 16; ++r) oacc[i][r] = 0.f;
   float m = -INFINITY, l = 0.f;
 
-  // LDS byte addresses of this lane's operand reads, computed once and held
-  // in registers (opaque to the compiler, which would otherwise recompute the
-  // swizzled offsets for every read): the K rows of each 16-wide d step, and
-  // the V columns of each 32-wide d block and row group.  The stage, the
-  // 32-key block and the 16-key step only add constants.
-  constexpr int NSD = D / 16, NDB = D / 32;
-  uint32_t ka[NSD], va[NDB][2];
-  {
-    const uint32_t kb = lds_offset(&Ks[0][0]), vb = lds_offset(&Vs[0][0]);
-#pragma unroll
-    for (int s = 0; s < NSD; ++s) {
-      ka[s] = kb + 2u * (uint32_t)(lr * D + 8 * ((2 * s + lh) ^ tile_swz<D>(lr)));
-      asm volatile("" : "+v"(ka[s]));
-    }
-    const int g = lane >> 4, q = lane & 15;
-#pragma unroll
-    for (int i = 0; i < NDB; ++i)
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        const int kk = 4 * (g >> 1) + 8 * hh + (q >> 2), col = 32 * i + 16 * (g & 1) + 4 * (q & 3);
-        va[i][hh] = vb + 2u * (uint32_t)(kk * D + 8 * ((col >> 3) ^ tile_swz<D>(kk)) + (col & 7));
-        asm volatile("" : "+v"(va[i][hh]));
-      }
-  }
+  // operand reads by per-lane LDS address (K rows, V^T columns); the stage,
+  // the array, the 32-key block and the 16-key step add constants
+  const FragAddr<D> fa(lds_offset(&Ks[0][0]), lane);
   constexpr uint32_t STAGE = BKV * D * 2;
-  // K fragment (as row_frag) of key block bb, d step s, stage ST
-  auto kfrag = [&](auto st_c, int bb, int s) -> u32x4 {
-    return *(const LDS_AS u32x4*)(size_t)(ka[s] + (uint32_t)(decltype(st_c)::value * STAGE + bb * 32 * D * 2));
-  };
-  // V^T fragment (as colt_frag) of d block i, key step s, stage ST
-  auto vfrag = [&](auto st_c, int i, int s) -> u32x4 {
-    u32x4 out;
-#pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-      const uint32_t a = va[i][hh] + (uint32_t)(decltype(st_c)::value * STAGE + s * 16 * D * 2);
-      const u32x2 w = __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS s16x4*)(size_t)a));
-      out[2 * hh] = w[0];
-      out[2 * hh + 1] = w[1];
-    }
-    return out;
-  };
+  const uint32_t v_minus_k = lds_offset(&Vs[0][0]) - lds_offset(&Ks[0][0]);
 
   sync_lds();
   // one 64-key tile in stage CUR (a constant: the loop below runs two per pass)
@@ -245,7 +252,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnShape sh, const bf
       for (int s = 0; s < D / 16; ++s)
 #pragma unroll
         for (int bb = 0; bb < BKV / 32; ++bb)
-          sacc[bb] = mfma32(kfrag(cur_c, bb, s), qf[s], sacc[bb]);
+          sacc[bb] = mfma32(fa.rows(s, cur * STAGE + bb * 32 * D * 2), qf[s], sacc[bb]);
       // lane holds query qrow, keys kv0 + 32bb + 8(r/4) + 4lh + r%4
       if (kv0 + BKV - 1 > wave_qmin) {
 #pragma unroll
@@ -282,7 +289,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnShape sh, const bf
       for (int s = 0; s < BKV / 16; ++s) {
         const u32x4 pf = pack_frag(sacc[s >> 1], 8 * (s & 1));
 #pragma unroll
-        for (int i = 0; i < D / 32; ++i) oacc[i] = mfma32(vfrag(cur_c, i, s), pf, oacc[i]);
+        for (int i = 0; i < D / 32; ++i)
+          oacc[i] = mfma32(fa.cols(i, v_minus_k + cur * STAGE + s * 16 * D * 2), pf, oacc[i]);
       }
     }
     sync_lds();
@@ -703,51 +711,21 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(AttnShape sh, const
 #pragma unroll
     for (int r = 0; r < 16; ++r) dq[i][r] = 0.f;
 
-  // LDS byte addresses of this lane's operand reads, computed once and held
-  // in registers the compiler cannot rematerialise: K and V rows (one layout)
-  // for each 16-wide d step, and K^T columns for each 32-wide d block and row
-  // group.  The tile's stage, the array, the 32-key block and the 16-key step
-  // only add constants.
-  uint32_t ra[NSD], ta[NI][2];
-  {
-    const uint32_t kb = lds_offset(&Ks[0][0]);
-#pragma unroll
-    for (int s = 0; s < NSD; ++s) {
-      ra[s] = kb + 2u * (uint32_t)(lr * D + 8 * ((2 * s + lh) ^ tile_swz<D>(lr)));
-      asm volatile("" : "+v"(ra[s]));
-    }
-    const int g = lane >> 4, q = lane & 15;
-#pragma unroll
-    for (int i = 0; i < NI; ++i)
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        const int kk = 4 * (g >> 1) + 8 * hh + (q >> 2), col = 32 * i + 16 * (g & 1) + 4 * (q & 3);
-        ta[i][hh] = kb + 2u * (uint32_t)(kk * D + 8 * ((col >> 3) ^ tile_swz<D>(kk)) + (col & 7));
-        asm volatile("" : "+v"(ta[i][hh]));
-      }
-  }
+  // operand reads by per-lane LDS address (K and V rows, K^T columns); the
+  // stage, the array, the 32-key block and the 16-key step add constants
+  const FragAddr<D> fa(lds_offset(&Ks[0][0]), lane);
   constexpr uint32_t STAGE = BKV * D * 2;
   const uint32_t v_minus_k = lds_offset(&Vs[0][0]) - lds_offset(&Ks[0][0]);
 
   // MFMA A operand of slot j of the tile in stage ST.
   auto operand = [&](auto j_c, auto st_c) -> u32x4 {
     constexpr int j = decltype(j_c)::value, st = decltype(st_c)::value;
-    if constexpr (j < 2 * PS) {  // row_frag of K (k even) or V (k odd)
+    if constexpr (j < 2 * PS) {  // rows of K (k even) or V (k odd)
       constexpr int bb = j / PS, k = j % PS;
-      const uint32_t a = ra[k >> 1] + (uint32_t)(st * STAGE + bb * 32 * D * 2) + ((k & 1) ? v_minus_k : 0u);
-      return *(const LDS_AS u32x4*)(size_t)a;
-    } else {  // colt_frag of K
+      return fa.rows(k >> 1, st * STAGE + bb * 32 * D * 2 + ((k & 1) ? v_minus_k : 0u));
+    } else {  // K^T columns
       constexpr int bb = (j - 2 * PS) / PQ, c = (j - 2 * PS) % PQ;
-      constexpr int i = c % NI, s = 2 * bb + c / NI;
-      u32x4 out;
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        const uint32_t a = ta[i][hh] + (uint32_t)(st * STAGE + s * 16 * D * 2);
-        const u32x2 w = __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS s16x4*)(size_t)a));
-        out[2 * hh] = w[0];
-        out[2 * hh + 1] = w[1];
-      }
-      return out;
+      return fa.cols(c % NI, st * STAGE + (2 * bb + c / NI) * 16 * D * 2);
     }
   };
 
