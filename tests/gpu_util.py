@@ -13,6 +13,7 @@ import pytest
 import torch
 
 from oracle import block as ob
+from paper_2510_02483_amd import configs
 
 OUT_TOL = 2e-2
 GRAD_TOL = 3e-2
@@ -54,3 +55,10 @@ def oracle_block(c, f):
 def bf16_randn(shape, seed, std=1.0, device="cuda"):
     g = torch.Generator().manual_seed(seed)
     return (torch.randn(shape, generator=g) * std).to(torch.bfloat16).to(device)
+
+
+# Many tokens, small weights: each weight-gradient product has 1-6 output tiles
+# of 256 x 256 and splits its 3000-deep contraction over 5 workgroups (the last
+# slice ragged), the partial sums reduced by a second kernel.
+LONG_NARROW = configs.BlockConfig("long-narrow", 18, batch=2, seq=1500, hidden=256, n_q_heads=4, n_kv_heads=2,
+                                  head_dim=64, intermediate=688, rope_theta=1e4)

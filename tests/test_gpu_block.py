@@ -6,7 +6,7 @@ import torch
 
 from paper_2510_02483_amd import configs, inputs, lib as L
 
-from gpu_util import GRAD_TOL, OUT_TOL, f64, fro_rel, max_rel, need_gpu, oracle_block, say
+from gpu_util import GRAD_TOL, LONG_NARROW, OUT_TOL, f64, fro_rel, max_rel, need_gpu, oracle_block, say
 
 pytestmark = pytest.mark.gpu
 
@@ -30,10 +30,6 @@ ONE_TOKEN = configs.BlockConfig("one-token", 16, batch=3, seq=1, hidden=256, n_q
                                 intermediate=688, rope_theta=1e4)
 D72 = configs.BlockConfig("d72", 15, batch=2, seq=96, hidden=288, n_q_heads=4, n_kv_heads=1, head_dim=72,
                           intermediate=392, rope_theta=5e5)
-# many tokens, small weights: each weight-gradient product has 1-6 output tiles
-# and splits its 3000-deep contraction over 5 workgroups (the last slice ragged)
-LONG_NARROW = configs.BlockConfig("long-narrow", 18, batch=2, seq=1500, hidden=256, n_q_heads=4, n_kv_heads=2,
-                                  head_dim=64, intermediate=688, rope_theta=1e4)
 
 BLOCK_CASES = [
     ("d104-gqa", D104_GQA, {"gamma": "random"}),

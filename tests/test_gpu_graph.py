@@ -13,7 +13,7 @@ import torch
 
 from paper_2510_02483_amd import configs, inputs, lib as L
 
-from gpu_util import need_gpu, say
+from gpu_util import LONG_NARROW, need_gpu, say
 
 pytestmark = pytest.mark.gpu
 
@@ -32,9 +32,9 @@ def _capture(step):
     return g
 
 
-def test_block_step_graph_replay():
+@pytest.mark.parametrize("c", [configs.TINY.with_(batch=2, seq=200), LONG_NARROW], ids=["tiny", "split-k"])
+def test_block_step_graph_replay(c):
     need_gpu()
-    c = configs.TINY.with_(batch=2, seq=200)
     say(f"graph capture {c}")
     blk = L.Block(c, inputs.make_inputs(c, gamma="random"))
     blk.step()
