@@ -282,7 +282,9 @@ int ls_rmsnorm_bwd(int64_t rows, int32_t hidden, const ls_bf16* x, const ls_bf16
  *   ls_gemm_nt:  C[M,N]  = A[M,K] . B[N,K]^T          (forward projection)
  *   ls_gemm_nn:  C[M,N]  = A[M,K] . B[K,N]            (input gradient)
  *   ls_gemm_tn:  C[M,N] (+)= A[K,M]^T . B[K,N], fp32  (weight gradient)
- * M, N, K > 0 and multiples of 8. */
+ * M, N, K > 0 and multiples of 8.  These single products take no workspace, so
+ * ls_gemm_tn never splits K over workgroups (the block and stack calls do, for
+ * weight gradients with few output tiles, in their workspace). */
 int ls_gemm_nt(int64_t M, int64_t N, int64_t K, const ls_bf16* A, const ls_bf16* B,
                ls_bf16* C, void* stream);
 int ls_gemm_nn(int64_t M, int64_t N, int64_t K, const ls_bf16* A, const ls_bf16* B,
@@ -318,7 +320,8 @@ int ls_embed_bwd(int64_t tokens, int32_t hidden, int32_t vocab, const int32_t* i
  * columns, where its epilogue allows) to minimise waves of workgroups times
  * tile area on the device's compute units.  ls_gemm_tile_override(bm, bn)
  * forces bm x bn (each 256 or 192) for every later launch in the process that
- * allows it (others keep 256 x 256); (0, 0) restores the automatic choice.
+ * allows it (others, and weight gradients that split K, keep 256 x 256);
+ * (0, 0) restores the automatic choice.
  * Process-wide setting, not tied to a stream.  Returns LS_ERR_SHAPE for
  * other sizes. */
 int ls_gemm_tile_override(int32_t bm, int32_t bn);
