@@ -491,9 +491,8 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnShape sh, con
   f32x4 Lq[2], Dq[2];  // base-2 log-sum-exp and D of the block's queries 8rq + 4lh + {0..3}, rq even / odd
   u32x4 pf[2], sf[2];
 
-  // One tile in stage ST (the next tile's stage is ST+1, the one after ST+2,
-  // modulo 3): the stage is a constant, so every LDS address is a per-lane
-  // offset plus an instruction offset.
+  // One tile in stage st; st1 and st2 are the stages of the next two tiles
+  // (the three rotate from tile to tile).
   auto tile = [&](int t, int st, int st1, int st2) {
     const int q0 = q_begin + (t % nqt) * BWD_BQ;
     // causal mask, on the tiles at the diagonal only (some query of the tile
