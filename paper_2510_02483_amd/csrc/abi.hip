@@ -215,7 +215,7 @@ ls::AttnShape attn_shape(const Dims& m) {
 
 // fp32 partial sums of the weight-gradient products that split K (their
 // output tiles alone would leave most compute units idle)
-int64_t kpart_floats(std::initializer_list<std::array<int64_t, 3>> shapes) {
+int64_t max_kpart_floats(std::initializer_list<std::array<int64_t, 3>> shapes) {
   int64_t n = 0;
   for (const auto& mnk : shapes) n = std::max(n, ls::gemm_kpart_floats((int)mnk[0], (int)mnk[1], (int)mnk[2]));
   return n;
@@ -239,7 +239,7 @@ AttnWs attn_ws_layout(const Dims& m) {
   w.dh1 = c.take(m.T * m.H * 2);
   w.partial = c.take(norm_partial_bytes(m));
   w.core = c.take(ls::attn_bwd_workspace(attn_shape(m)));
-  w.kpart_floats = kpart_floats({{m.H, m.Pq, m.T}, {m.Pqkv, m.H, m.T}});  // dWo, dWqkv
+  w.kpart_floats = max_kpart_floats({{m.H, m.Pq, m.T}, {m.Pqkv, m.H, m.T}});  // dWo, dWqkv
   w.kpart = c.take((size_t)w.kpart_floats * 4);
   w.total = c.off;
   return w;
@@ -255,7 +255,7 @@ MlpWs mlp_ws_layout(const Dims& m) {
   w.dgu = c.take(m.T * 2 * m.I * 2);
   w.dh2 = c.take(m.T * m.H * 2);
   w.partial = c.take(norm_partial_bytes(m));
-  w.kpart_floats = kpart_floats({{m.H, m.I, m.T}, {2 * m.I, m.H, m.T}});  // dWd, dWg/dWu
+  w.kpart_floats = max_kpart_floats({{m.H, m.I, m.T}, {2 * m.I, m.H, m.T}});  // dWd, dWg/dWu
   w.kpart = c.take((size_t)w.kpart_floats * 4);
   w.total = c.off;
   return w;
