@@ -88,7 +88,23 @@ def cpu_baseline(c, sequences: int):
     return {"value": flops.block_fwd_bwd_flops(sample) / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads),
             "kind": "oracle",
             "sample": f"{n} of {c.batch} sequences ({n * c.seq} tokens) of the same block, fp64 numpy oracle "
-                      f"(BLAS matmuls), {dt:.1f} s wall"}
+                      f"(BLAS matmuls), {dt:.1f} s wall",
+            "host": host_record()}
+
+
+def host_record() -> dict:
+    """The CPU the oracle ran on: logical CPUs visible to this process, the
+    machine's count and the model name."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"nproc": len(os.sched_getaffinity(0)), "cpu_count": os.cpu_count(), "cpu_model": model}
 
 
 def kernel_only(args):

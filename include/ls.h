@@ -73,7 +73,10 @@ typedef enum {
  * (sizes other than 64 and 128, such as the 104 of a 64-head 6656-wide model,
  * run in 128-wide slots: each head's two RoPE halves are placed at slot
  * offsets 0 and 64 with zero features between, which changes no result);
- * hidden and intermediate are multiples of 8; rms_eps >= 0, rope_theta > 1. */
+ * hidden and intermediate are multiples of 8; rms_eps >= 0, rope_theta > 1.
+ * hidden need not equal n_q_heads*head_dim: the query/output projections map
+ * hidden <-> n_q_heads*head_dim features either way (e.g. hidden 384 with
+ * 4 heads of 64 or 6 heads of 128). */
 typedef struct {
   int32_t batch;
   int32_t seq;
@@ -121,7 +124,9 @@ int ls_attn_fwd(const ls_block_cfg* cfg, const ls_bf16* x, const ls_block_weight
                 ls_bf16* x2, void* attn_saved, void* workspace, size_t workspace_bytes,
                 void* stream);
 
-/* Attention sub-layer backward.  Given dx2 = dL/dx2, writes dx = dL/dx =
+/* Attention sub-layer backward (Section 1: the backward pass of the attention
+ * layer is one of the operations the report's algorithmic step optimises;
+ * Section 2.4 names the layer).  Given dx2 = dL/dx2, writes dx = dL/dx =
  * dx2 + (d/dx of the attention branch)^T dx2 and the gradients of attn_norm,
  * wq, wk, wv, wo (other members of *g are ignored and may be NULL).  The
  * backward recomputes the softmax from the saved log-sum-exp.  x and
@@ -139,15 +144,19 @@ int ls_mlp_fwd(const ls_block_cfg* cfg, const ls_bf16* x2, const ls_block_weight
                ls_bf16* y, void* mlp_saved, void* workspace, size_t workspace_bytes,
                void* stream);
 
-/* MLP sub-layer backward: dx2 = dy + (d/dx2 of the MLP branch)^T dy and the
- * gradients of mlp_norm, wg, wu, wd. */
+/* MLP sub-layer backward (Section 1: the backward pass of the MLP layer is one
+ * of the operations the report's algorithmic step optimises; Section 2.4 names
+ * the layer): dx2 = dy + (d/dx2 of the MLP branch)^T dy and the gradients of
+ * mlp_norm, wg, wu, wd. */
 int ls_mlp_bwd(const ls_block_cfg* cfg, const ls_bf16* x2, const ls_block_weights* w,
                const void* mlp_saved, const ls_bf16* dy, ls_bf16* dx2,
                const ls_block_grads* g, int accumulate, void* workspace,
                size_t workspace_bytes, void* stream);
 
-/* Whole block, forward then backward, in one call: writes y, dx and all nine
- * weight gradients for upstream gradient dy.  workspace: block_workspace bytes. */
+/* Whole block, forward then backward, in one call (Section 1: the forward and
+ * backward pass operations of the attention and MLP layers; Section 2.4: the
+ * block): writes y, dx and all nine weight gradients for upstream gradient dy.
+ * workspace: block_workspace bytes. */
 int ls_block_fwd_bwd(const ls_block_cfg* cfg, const ls_bf16* x, const ls_block_weights* w,
                      const ls_bf16* dy, ls_bf16* y, ls_bf16* dx, const ls_block_grads* g,
                      int accumulate, void* workspace, size_t workspace_bytes, void* stream);
@@ -217,7 +226,8 @@ int ls_stack_fwd_bwd(const ls_stack_cfg* cfg, const int32_t* ids, const int32_t*
 /* ---- optimizer step ------------------------------------------------------------
  *
  * The report trains with AdamW (beta1 0.9, beta2 0.95, weight decay 0.01) and
- * gradient clipping at global norm 1.0 (Section 2.4, Table 2).  One step over
+ * gradient clipping at global norm 1.0 (Section 2.5, optimizer settings, and Table
+ * 2).  One step over
  * n parameters held in flat fp32 arrays (callers lay every tensor out in one
  * arena; the first n_decay parameters take weight decay, the rest -- RMSNorm
  * gains -- do not):

@@ -6,7 +6,7 @@ links or calls this module; only the tests, the smoke check and the CPU
 baseline leg of the benchmark do.
 
 The Litespark report trains with AdamW (beta1 0.9, beta2 0.95, weight decay
-0.01) and clips gradients at norm 1.0 (Section 2.4, Table 2).  The step, over
+0.01) and clips gradients at norm 1.0 (Section 2.5, optimizer settings, and Table 2).  The step, over
 all parameters held in flat arrays, of which the first n_decay take weight
 decay and the rest (RMSNorm gains) do not:
 

@@ -30,6 +30,17 @@ ONE_TOKEN = configs.BlockConfig("one-token", 16, batch=3, seq=1, hidden=256, n_q
                                 intermediate=688, rope_theta=1e4)
 D72 = configs.BlockConfig("d72", 15, batch=2, seq=96, hidden=288, n_q_heads=4, n_kv_heads=1, head_dim=72,
                           intermediate=392, rope_theta=5e5)
+# hidden != n_q_heads * head_dim: the query/output projections narrow (384 -> 256
+# features) or widen (256 -> 768) the model width
+NARROW_HEADS = configs.BlockConfig("narrow-heads", 19, batch=2, seq=136, hidden=384, n_q_heads=4, n_kv_heads=2,
+                                   head_dim=64, intermediate=1040, rope_theta=1e4)
+WIDE_HEADS = configs.BlockConfig("wide-heads", 20, batch=1, seq=200, hidden=256, n_q_heads=6, n_kv_heads=2,
+                                 head_dim=128, intermediate=688, rope_theta=5e5)
+# multi-head attention with 64-wide heads: one query head per kv head, so the
+# dK/dV kernel never splits a group (its unsplit 64-wide variant, with the
+# inverse RoPE on the dK store)
+MHA_D64 = configs.BlockConfig("mha-d64", 21, batch=2, seq=200, hidden=256, n_q_heads=4, n_kv_heads=4, head_dim=64,
+                              intermediate=520, rope_theta=1e4)
 
 BLOCK_CASES = [
     ("d104-gqa", D104_GQA, {"gamma": "random"}),
@@ -43,6 +54,10 @@ BLOCK_CASES = [
     ("mid-d128", MID_D128, {}),
     ("mha-d128-sharp", MHA_D128, {"wq_std": 0.3}),
     ("long-narrow", LONG_NARROW, {"gamma": "random"}),
+    ("hidden-384-heads-4x64", NARROW_HEADS, {"gamma": "random"}),
+    ("hidden-256-heads-6x128-sharp", WIDE_HEADS, {"wq_std": 0.3}),
+    ("mha-d64", MHA_D64, {"gamma": "random"}),
+    ("mha-d64-sharp", MHA_D64, {"wq_std": 0.4}),
 ]
 
 
@@ -80,7 +95,8 @@ def test_block_parity(name, c, kw):
     compare_block(c, blk, fwd, gr)
 
 
-@pytest.mark.parametrize("c", [MID_D64, D104_GQA, LONG_NARROW], ids=["d64", "d104-padded", "split-k"])
+@pytest.mark.parametrize("c", [MID_D64, D104_GQA, LONG_NARROW, NARROW_HEADS, WIDE_HEADS],
+                         ids=["d64", "d104-padded", "split-k", "hidden-384-heads-4x64", "hidden-256-heads-6x128"])
 def test_sublayers_match_block_call(c):
     """ls_attn_fwd / ls_mlp_fwd / ls_mlp_bwd / ls_attn_bwd chained by hand give
     the oracle's intermediates (x2, dx2) and final results (also with heads of
@@ -138,36 +154,27 @@ def test_accumulate_and_side_stream(c):
     compare_block(c, blk, fwd, {**gr, **{n: 2 * gr[n] for n in GRAD_NAMES}})
 
 
-def test_block_3b_full_size_sampled():
-    """The Llama-3.2-3B-shaped block at its full size (batch 4 x seq 2048), in
-    the launch configuration the benchmark times.  The oracle computes
-    sequence 0 in full; the upstream gradient is zero on sequences 1..3 so
-    that every weight gradient is sequence 0's alone, and sequences 1..3 are
-    checked by permuting the batch (sequences are independent)."""
-    need_gpu()
-    c = configs.B3
-    say(f"3b full size {c}")
+def _full_parity(c):
+    """The block at its full size and launch configuration, every sequence
+    with its own upstream gradient, against the oracle on the whole batch:
+    y and dx of every token and each weight gradient over all batch x seq
+    rows of its contraction."""
     host = inputs.make_inputs(c)
-    host["dy"][1:] = 0
     blk = L.Block(c, host)
     blk.step()
     torch.cuda.synchronize()
-    y_all = blk.y.clone()
-    one = c.with_(batch=1)
-    f = inputs.to_f64({k: (v[:1] if k in ("x", "dy") else v) for k, v in host.items()})
-    say("  oracle on sequence 0 ...")
-    fwd, gr = oracle_block(one, f)
-    compare_block(c, blk, fwd, gr, sample=slice(0, 1))
-    # permuting the batch permutes the outputs
-    perm = [2, 0, 3, 1]
-    host2 = dict(host)
-    host2["x"] = host["x"][perm].contiguous()
-    blk2 = L.Block(c, host2)
-    blk2.step()
-    torch.cuda.synchronize()
-    ya = f64(y_all).reshape(4, c.seq, c.hidden)[perm]
-    yb = f64(blk2.y).reshape(4, c.seq, c.hidden)
-    assert np.array_equal(ya, yb)
+    say(f"  oracle on the whole batch ({c.batch} x {c.seq}) ...")
+    fwd, gr = oracle_block(c, inputs.to_f64(host))
+    compare_block(c, blk, fwd, gr)
+
+
+def test_block_3b_full_size():
+    """The Llama-3.2-3B-shaped block at its full size (batch 4 x seq 2048):
+    the benchmark's workload and launch configuration, compared in full."""
+    need_gpu()
+    c = configs.B3
+    say(f"3b full size {c}")
+    _full_parity(c)
 
 
 def _prefix_parity(c, t0, sample_seq=0):
@@ -216,22 +223,13 @@ def test_block_3b_8k_full_size_prefix():
     _prefix_parity(c, 1024)
 
 
-def test_block_30b_full_size_prefix():
+def test_block_30b_full_size():
     """The Llama-30B-shaped block (batch 2 x seq 2048, 52 MHA heads, SwiGLU
-    17920) at full size; oracle on the first 512 tokens of sequence 1, and the
-    batch swapped gives the outputs swapped exactly."""
+    17920) at full size, compared in full."""
     need_gpu()
     c = configs.B30
     say(f"30b full size {c}")
-    blk, host = _prefix_parity(c, 512, sample_seq=1)
-    y_all = f64(blk.y).reshape(c.batch, c.seq, c.hidden)
-    del blk
-    host2 = dict(host)
-    host2["x"] = host["x"][[1, 0]].contiguous()
-    blk2 = L.Block(c, host2)
-    blk2.step()
-    torch.cuda.synchronize()
-    assert np.array_equal(y_all[[1, 0]], f64(blk2.y).reshape(c.batch, c.seq, c.hidden))
+    _full_parity(c)
 
 
 def test_block_paper_3b_full_size_prefix():

@@ -96,6 +96,8 @@ ATTN_CASES = [
     ("sharp-d128", 2, 130, 4, 4, 128, math.sqrt(3.0)),
     ("sharp-d64-long", 1, 520, 6, 3, 64, math.sqrt(3.0)),
     ("single-token", 3, 1, 2, 1, 128, 1.0),
+    ("mha-d64", 2, 200, 4, 4, 64, 1.0),
+    ("mha-d64-sharp", 1, 264, 3, 3, 64, math.sqrt(3.0)),
 ]
 
 
@@ -139,10 +141,13 @@ def test_attention_core(name, B, S, nq, nkv, d, std):
 SAMPLED_GROUP_CASES = [
     # name, batch, seq, nq, nkv, d, kv head checked.  The dK/dV kernel splits a
     # kv head's query-head group over workgroups when (seq/128) * nkv * batch
-    # is below 512: "8k" fills the chip unsplit (512 workgroups); "split2of4"
-    # (256 workgroups, groups of 4) sums two partials of two heads each.
+    # is below 512: "8k" and "d64-unsplit" fill the chip unsplit (512
+    # workgroups); "split2of4" (256 workgroups, groups of 4) sums two partials
+    # of two heads each.
     ("8k", 1, 8192, 24, 8, 128, 5),
     ("split2of4", 1, 2048, 64, 16, 64, 11),
+    # 64-wide heads at (2048/128) * 8 * 4 = 512 workgroups: the unsplit kernel
+    ("d64-unsplit", 4, 2048, 32, 8, 64, 6),
 ]
 
 

@@ -205,30 +205,32 @@ def test_stack_tiny_explicit_targets_and_depth():
     compare_stack(st, oracle_stack(sc, host, targets=tg))
 
 
-def test_stack_3b_full_size_prefix():
+def test_stack_3b_full_size_sequence():
     """The 3B model's shapes (hidden 3072, 24/8 heads, SwiGLU 8192, vocabulary
     128256, micro-batch 4 x 2048) at depth 2, in the launch configuration of
-    the full model.  Targets only on the first t0 tokens of sequence 1: the
-    loss and every gradient then equal those of the t0-token problem (causal
-    blocks; zero dz elsewhere), which the oracle computes; the other rows'
-    losses are exactly zero.  The same step without recomputation gives the
-    same loss and gradients bit for bit."""
+    the full model.  Next-token targets on every position of sequence 1 (all
+    2047 of them) and none elsewhere: the loss and every gradient then equal
+    those of that one 2048-token sequence (the other sequences get no
+    gradient), which the oracle computes in full; the other rows' losses are
+    exactly zero.  The same step without recomputation gives the same loss
+    and gradients bit for bit."""
     need_gpu()
     sc = configs.STACK_3B.with_(n_layers=2)
-    t0, b = 256, 1
-    say(f"stack full-size prefix {sc} t0={t0}")
-    host = inputs.make_stack_inputs(sc, e_std=0.1)
+    b = 1
     S = sc.block.seq
+    t0 = S - 1
+    say(f"stack full-size sequence {sc} b={b}")
+    host = inputs.make_stack_inputs(sc, e_std=0.1)
     tg = torch.full((sc.block.batch, S), -1, dtype=torch.int32)
     tg[b, :t0] = host["ids"][b, 1:t0 + 1]
     tg = tg.reshape(-1)
     st = L.Stack(sc, host, targets=tg)
     st.step()
     torch.cuda.synchronize()
-    say("  gpu done; oracle on the prefix")
-    ref = oracle_stack(sc, host, targets=tg, batch_rows=(b, t0))
+    say("  gpu done; oracle on the whole sequence")
+    ref = oracle_stack(sc, host, targets=tg, batch_rows=(b, S))
     sel = np.zeros(sc.tokens, dtype=bool)
-    sel[b * S:b * S + t0] = True
+    sel[b * S:(b + 1) * S] = True
     assert np.all(f64(st.row_loss)[~sel] == 0.0)
     compare_stack(st, ref, rows_sel=sel)
     loss1 = st.loss.clone()
