@@ -274,6 +274,24 @@ int ls_attn_core_bwd(const ls_block_cfg* cfg, const ls_bf16* qkv, const ls_bf16*
                      const float* lse, const ls_bf16* dout, ls_bf16* dqkv, void* workspace,
                      size_t workspace_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * computation and kernels as ls_attn_core_bwd, bit for bit, without a
+ * workspace argument.  Its scratch is a device array the library owns,
+ * LS_ATTN_CORE_BWD_NOALLOC_SCRATCH bytes on every GPU the library runs on,
+ * held until the process ends.  The call allocates nothing (no hipMalloc,
+ * hipFree or allocating library routine).  A shape whose workspace
+ * (ls_attn_core_bwd_workspace) exceeds the array fails with
+ * LS_ERR_WORKSPACE before any HIP call.  Every call on a GPU shares that GPU's
+ * array (it runs on the current device): calls that overlap on one GPU, on
+ * different streams or from different threads, race and give wrong results;
+ * calls ordered on one stream are safe.  The first call on a device looks the
+ * array's device address up (hipGetSymbolAddress); errors there return
+ * LS_ERR_HIP. */
+#define LS_ATTN_CORE_BWD_NOALLOC_SCRATCH ((size_t)16 << 20)
+int ls_attn_core_bwd_noalloc(const ls_block_cfg* cfg, const ls_bf16* qkv, const ls_bf16* o,
+                             const float* lse, const ls_bf16* dout, ls_bf16* dqkv, void* stream);
+
 /* RMSNorm over rows of length `hidden`: h = x * r * gamma, r = (mean x^2 + eps)^-1/2.
  * x, h: [rows, hidden] bf16; r: [rows] fp32. */
 int ls_rmsnorm_fwd(int64_t rows, int32_t hidden, float eps, const ls_bf16* x,

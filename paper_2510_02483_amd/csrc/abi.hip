@@ -930,6 +930,64 @@ int ls_attn_core_bwd(const ls_block_cfg* cfg, const ls_bf16* qkv, const ls_bf16*
   return LS_OK;
 }
 
+// ---- attention-core backward with library-owned scratch ----------------------------
+//
+// ls_attn_core_bwd_noalloc runs the kernels of ls_attn_core_bwd with their
+// scratch (D, the base-2 log-sum-exp and, when the dK/dV group is split, the
+// partial dK | dV rows) in this file-scope device array instead of a
+// caller-provided workspace.  Every GPU the library runs on holds its own
+// copy until the process ends.  In host code `scratch` names a host-side
+// stand-in, not device memory: its device address is looked up once per
+// device (hipGetSymbolAddress with that device current) and only that address
+// is handed to kernels.  The kernels write every scratch value before they
+// read it, so nothing is cleared between calls.
+static __device__ __align__(256) unsigned char scratch[LS_ATTN_CORE_BWD_NOALLOC_SCRATCH];
+
+static constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static void* g_scratch_addr[kMaxDevices] = {};
+
+// Device address of `scratch` on the current device (looked up on the first
+// call on each device).
+static int scratch_address(void** out) {
+  int dev = -1;
+  LS_HIP(hipGetDevice(&dev), "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(LS_ERR_UNSUPPORTED, "device index %d beyond %d", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_addr[dev]) {
+    void* p = nullptr;
+    LS_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(LS_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_addr[dev] = p;
+  }
+  *out = g_scratch_addr[dev];
+  return LS_OK;
+}
+
+int ls_attn_core_bwd_noalloc(const ls_block_cfg* cfg, const ls_bf16* qkv, const ls_bf16* o, const float* lse,
+                             const ls_bf16* dout, ls_bf16* dqkv, void* stream) {
+  if (int e = check_core_cfg(cfg)) return e;
+  const Dims m = dims_of(*cfg);
+  const size_t need = ls::attn_bwd_workspace(attn_shape(m));
+  std::vector<Range> in{{qkv, (size_t)(m.T * m.Dqkv * 2), "qkv"},
+                        {o, (size_t)(m.T * m.Dq * 2), "o"},
+                        {lse, (size_t)(m.B * m.nq * m.S * 4), "lse"},
+                        {dout, (size_t)(m.T * m.Dq * 2), "dout"}};
+  std::vector<Range> out{{dqkv, (size_t)(m.T * m.Dqkv * 2), "dqkv"}};
+  if (int e = check_ranges(in, out)) return e;
+  if (need > (size_t)LS_ATTN_CORE_BWD_NOALLOC_SCRATCH)
+    return fail(LS_ERR_WORKSPACE,
+                "this shape needs %zu bytes of scratch, beyond the library's %zu-byte array (use ls_attn_core_bwd "
+                "with a workspace)",
+                need, (size_t)LS_ATTN_CORE_BWD_NOALLOC_SCRATCH);
+  void* ws = nullptr;
+  if (int e = scratch_address(&ws)) return e;
+  LS_HIP(ls::attn_bwd(attn_shape(m), (const bf16_t*)qkv, (const bf16_t*)o, lse, (const bf16_t*)dout, (bf16_t*)dqkv,
+                      nullptr, ws, (hipStream_t)stream),
+         "attention backward");
+  return LS_OK;
+}
+
 static int check_norm_shape(int64_t rows, int32_t hidden) {
   if (rows <= 0 || hidden <= 0) return fail(LS_ERR_SHAPE, "rows and hidden must be positive");
   if (hidden % 8) return fail(LS_ERR_SHAPE, "hidden %d is not a multiple of 8", hidden);

@@ -82,6 +82,7 @@ _PROTOS = {
     "ls_attn_core_fwd": (ctypes.c_int, [_P, _P, _P, _P, _P]),
     "ls_attn_core_bwd_workspace": (ctypes.c_size_t, [_P]),
     "ls_attn_core_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "ls_attn_core_bwd_noalloc": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P]),
     "ls_rmsnorm_fwd": (ctypes.c_int, [ctypes.c_int64, ctypes.c_int32, ctypes.c_float, _P, _P, _P, _P, _P]),
     "ls_rmsnorm_bwd_workspace": (ctypes.c_size_t, [ctypes.c_int64, ctypes.c_int32]),
     "ls_rmsnorm_bwd": (ctypes.c_int, [ctypes.c_int64, ctypes.c_int32, _P, _P, _P, _P, _P, _P, _P, ctypes.c_int, _P,
@@ -209,6 +210,15 @@ def ls_attn_core_bwd(c, qkv, o, lse, dout, dqkv, workspace, stream=None):
     cfg = make_cfg(c)
     _check(lib().ls_attn_core_bwd(ctypes.byref(cfg), _p(qkv), _p(o), _p(lse), _p(dout), _p(dqkv), _p(workspace),
                                   workspace.numel() * workspace.element_size(), _stream(stream)), "ls_attn_core_bwd")
+
+
+NOALLOC_SCRATCH_BYTES = 16 << 20  # LS_ATTN_CORE_BWD_NOALLOC_SCRATCH
+
+
+def ls_attn_core_bwd_noalloc(c, qkv, o, lse, dout, dqkv, stream=None):
+    cfg = make_cfg(c)
+    _check(lib().ls_attn_core_bwd_noalloc(ctypes.byref(cfg), _p(qkv), _p(o), _p(lse), _p(dout), _p(dqkv),
+                                          _stream(stream)), "ls_attn_core_bwd_noalloc")
 
 
 def ls_rmsnorm_fwd(rows, hidden, eps, x, gamma, h, r, stream=None):

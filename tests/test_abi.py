@@ -276,3 +276,22 @@ def test_size_limits():
     V = ctypes.c_void_p
     assert lib.ls_cross_entropy(1 << 31, 1, 8, V(1 << 32), V(1 << 33), None, V(1 << 34), V(1 << 35),
                                 V(1 << 36), 1 << 40, None) == 2
+
+
+def test_attn_core_bwd_noalloc_argument_checks():
+    """The no-allocation attention backward checks its arguments and its
+    scratch limit before any HIP call (so these run without a GPU)."""
+    lib = L.lib()
+    V = ctypes.c_void_p
+    small = cfg_of(configs.TINY)
+    big = cfg_of(configs.PAPER_3B)   # its split dK/dV partials exceed the library's scratch array
+    assert L.ls_attn_core_bwd_workspace(configs.PAPER_3B) > L.NOALLOC_SCRATCH_BYTES
+    assert L.ls_attn_core_bwd_workspace(configs.TINY) <= L.NOALLOC_SCRATCH_BYTES
+    qkv, o, lse, do, dqkv = (1 << 36), (1 << 37), (1 << 38), (1 << 39), (1 << 40)
+    assert lib.ls_attn_core_bwd_noalloc(ctypes.byref(big), V(qkv), V(o), V(lse), V(do), V(dqkv), None) == 6
+    assert "scratch" in lib.ls_last_error().decode()
+    assert lib.ls_attn_core_bwd_noalloc(ctypes.byref(small), V(qkv), V(o), None, V(do), V(dqkv), None) == 1
+    assert lib.ls_attn_core_bwd_noalloc(ctypes.byref(small), V(qkv), V(o), V(lse), V(do), V(qkv), None) == 5
+    assert lib.ls_attn_core_bwd_noalloc(ctypes.byref(small), V(qkv), V(o), V(lse), V(do), V(dqkv + 8), None) == 4
+    odd = cfg_of(configs.TINY.with_(head_dim=104, hidden=416))
+    assert lib.ls_attn_core_bwd_noalloc(ctypes.byref(odd), V(qkv), V(o), V(lse), V(do), V(dqkv), None) == 3
