@@ -1,12 +1,14 @@
 // bf16 matrix products on gfx950 matrix cores (v_mfma_f32_32x32x16_bf16) with
 // fp32 accumulation and fused epilogues for the decoder block.
 //
-// One workgroup of 4 waves computes a BM x BN tile of C (256 or 192 on each
-// side); each wave owns a quarter (up to 16 MFMA blocks of 32x32, accumulators
-// in AGPRs).  Operand tiles of 64 k-values move global -> LDS with buffer loads
-// that write LDS directly (16 bytes per lane, no staging registers) and return
-// zero outside the operand, so ragged edges need no branches.  Two LDS stages
-// of 64 KB: tile k+1 is in flight while the matrix cores consume tile k.
+// One workgroup of 4 waves (one per SIMD, 2 x 2 wave tiles) or 8 waves (two
+// per SIMD, 4 x 2) computes a BM x BN tile of C (256 or 192 on each side);
+// each wave owns up to 16 MFMA blocks of 32x32 with their accumulators in
+// registers.  Operand tiles of 64 k-values move global -> LDS with buffer
+// loads that write LDS directly (16 bytes per lane, no staging registers)
+// and return zero outside the operand, so ragged edges need no branches.  Two
+// LDS stages of about 64 KB: tile k+1 is in flight while the matrix cores
+// consume tile k.
 //
 // The tile shape is picked per launch: on 256 compute units an 8192 x 3072
 // output is 384 tiles of 256 x 256 (one and a half waves of workgroups) but
@@ -18,10 +20,17 @@
 // pieces at well over one and a half times the rate of 64-byte ones (each
 // piece is one L1->L2 request and the number of requests in flight is capped).
 //
-// LDS layouts (no padding; an XOR swizzle of the 16-byte chunk index keeps
-// the fragment reads free of bank conflicts):
-//   k-contiguous operand  [256 rows][64 k]  128-byte rows, chunk c of row r at
-//                         slot c ^ ((r/2) % 8); fragments are 16-byte reads.
+// LDS layouts (the fragment reads are free of bank conflicts):
+//   k-contiguous operand  1 KB blocks of 8 rows x 64 k, KC_PITCH = 1040 bytes
+//                         apart (16 bytes of padding): block (r % 8) + 8 (r / 64)
+//                         holds the rows of one 64-row segment that are equal
+//                         mod 8, row r at 128-byte position (r / 8) % 8.  A
+//                         block's load reads each row's 128 bytes with 8
+//                         consecutive lanes in order; the 16 consecutive rows
+//                         a 16-lane group reads at one k step fall on 16
+//                         distinct 16-byte bank groups (padding and the mod-8
+//                         interleave); fragments are 16-byte reads at a
+//                         per-lane base plus constant offsets.
 //   k-strided operand     [64 k][W cols]: for W = 256, k-rows 2j and 2j+1 fill
 //                         the 1 KB block j (at bytes 0 and 512); for W = 192,
 //                         block 8g + b holds k-rows 8b .. 8b+7 of the 64-column
@@ -51,8 +60,8 @@ namespace {
 
 constexpr int KT = 64;                      // tile depth
 constexpr int KSTEPS = KT / 16;             // MFMA k-steps per tile
-constexpr int NT = 256;                     // 4 waves, 2 x 2 over the tile
-constexpr int TILE_ELEMS = 256 * KT;        // LDS region of one operand tile (32 KB)
+constexpr int TILE_ELEMS = 256 * KT;        // LDS region of one k-strided operand tile (32 KB)
+constexpr int KC_PITCH = 1040;              // bytes per 1 KB block of a k-contiguous tile (16 B of padding)
 constexpr int GROUP_M = 8;                  // tile rows per group in the launch order
 constexpr int EPI_ROPE64 = 100;             // EPI_ROPE for 64-wide heads
 constexpr uint32_t OOB = LS_OOB;
@@ -93,7 +102,10 @@ LS_DEV void map_tile(int wg, int tiles_m, int tiles_n, int& tm, int& tn) {
 //    64-byte runs on distinct quarters.  With W = 192 the rows of a block are
 //    128 bytes apart (window offsets 0, 128, 0, 128), and XOR with
 //    4 * ((k/2) % 2) moves the second pair by 64 bytes.
-LS_DEV int kc_swz(int r) { return (r >> 1) & 7; }
+// Byte offset of tile row r in a k-contiguous tile: block (r % 8) + 8 (r / 64)
+// of KC_PITCH bytes holds the 8 rows of one 64-row segment that are equal
+// mod 8, at 128-byte positions (r / 8) % 8.
+LS_DEV constexpr int kc_row_off(int r) { return ((r & 7) | ((r >> 6) << 3)) * KC_PITCH + ((r >> 3) & 7) * 128; }
 template <int W>
 LS_DEV int ks_swz(int k) {
   return W == 256 ? 4 * (k & 3) : 4 * ((k >> 1) & 1);
@@ -104,11 +116,11 @@ LS_DEV int ks_off(int kk, int col) {
   if constexpr (W == 256) return (kk >> 1) * 512 + (kk & 1) * W + 8 * ((col >> 3) ^ ks_swz<W>(kk)) + (col & 7);
   else return ((col >> 6) * 8 + (kk >> 3)) * 512 + (kk & 7) * 64 + 8 * (((col & 63) >> 3) ^ ks_swz<W>(kk)) + (col & 7);
 }
-// Load instructions (1 KB blocks) per wave for a k-strided tile of width W, and
+// 1 KB blocks (one load instruction each) of a k-strided tile of width W, and
 // the first k-row of block j.
 template <int W>
-constexpr int ks_loads() {
-  return W == 256 ? 8 : 6;
+constexpr int ks_blocks() {
+  return W == 256 ? 32 : 24;
 }
 template <int W>
 LS_DEV int ks_row0(int j) {
@@ -142,27 +154,30 @@ struct OpLoads {
   uint32_t kpos[2];   // k-contiguous: 8c for even / odd blocks; k-strided: the lane's k-row in its block
 };
 
-LS_DEV int kc_chunk(int j, int lane) { return (lane & 7) ^ kc_swz(8 * j + (lane >> 3)); }
-
-// k-contiguous operand: tile rows of this wave map to rows lrow0 .. of a
-// resource of `lrows` rows at `base` (leading dimension ld elements).
+// k-contiguous operand.  Block j of the tile holds rows 64 (j / 8) + j % 8 +
+// 8 i (i = 0..7): lane l of its load reads 16 bytes (k = k0 + 8 (l % 8) ..)
+// of row i = l / 8 and writes them at 16 l of the block, so the lanes of a
+// row read its 128 bytes in order.  The wave's blocks jb .. jb+NL-1 start at
+// row res_row0 of a resource of `lrows` rows at `base` (leading dimension ld
+// elements); when they span two 64-row segments the resource is one buffer.
 template <int NL>
-LS_DEV void kc_setup(OpLoads<NL>& o, const void* base, int lrow0, int lrows, int64_t ld, int lane) {
+LS_DEV void kc_setup(OpLoads<NL>& o, const void* base, int res_row0, int lrows, int64_t ld, int lane, int jb) {
   o.r = rsrc(base, clamp_bytes((int64_t)lrows * ld * 2));
 #pragma unroll
   for (int l = 0; l < NL; ++l) {
-    const int lr = lrow0 + 8 * l + (lane >> 3);
-    o.voff[l] = lr < lrows ? (uint32_t)((int64_t)lr * ld * 2 + 16 * kc_chunk(l, lane)) : OOB;
+    const int j = jb + l;
+    const int lr = res_row0 + 64 * ((j >> 3) - (jb >> 3)) + (j & 7) + 8 * (lane >> 3);
+    o.voff[l] = lr < lrows ? (uint32_t)((int64_t)lr * ld * 2 + 16 * (lane & 7)) : OOB;
   }
-  o.kpos[0] = 8 * kc_chunk(0, lane);
-  o.kpos[1] = 8 * kc_chunk(1, lane);
+  o.kpos[0] = 8 * (lane & 7);
+  o.kpos[1] = 8 * (lane & 7);
 }
 
 // k-strided operand: columns col0 .. col0 + W - 1 of `cols`; the k rows are
 // placed by the scalar offset (and the resource) of each tile.
-template <int NL, int W>
+template <int NL, int W, int NW>
 LS_DEV void ks_setup(OpLoads<NL>& o, int col0, int cols, int64_t ld, int wave, int lane) {
-  static_assert(NL == ks_loads<W>(), "one load per 1 KB block");
+  static_assert(NL * NW == ks_blocks<W>(), "one load per 1 KB block");
   constexpr int CPR = W == 256 ? 32 : 8;  // lanes per k-row
   const int sub = lane / CPR;              // the lane's k-row within its block
 #pragma unroll
@@ -190,12 +205,14 @@ LS_DEV uint32_t load_off(const OpLoads<NL>& o, int l, int kvalid, int wave) {
 // (m0: the wave's first block of the stage).
 template <bool KC, int NL, int W>
 LS_DEV void load_one(const OpLoads<NL>& o, int l, uint32_t soff, int kvalid, uint32_t m0, int wave) {
-  dma1(o.r, load_off<KC, NL, W>(o, l, kvalid, wave), soff, m0 + 1024u * l);
+  dma1(o.r, load_off<KC, NL, W>(o, l, kvalid, wave), soff, m0 + (KC ? (uint32_t)KC_PITCH : 1024u) * l);
 }
 
-// Fragment of a k-contiguous tile: lane gets row `r` (tile-local), k = 16s + 8*(lane/32) .. +7.
-LS_DEV u32x4 frag_kc(const bf16_t* lds, int r, int s, int lh) {
-  return *(const u32x4*)(lds + r * KT + 8 * ((2 * s + lh) ^ kc_swz(r)));
+// Fragment of a k-contiguous tile (at byte address t): lane gets row `r`
+// (tile-local), k = 16s + 8*(lane/32) .. +7.  The 16 rows a 16-lane group
+// reads at one k step sit in 16 distinct 16-byte bank groups.
+LS_DEV u32x4 frag_kc(const char* t, int r, int s, int lh) {
+  return *(const u32x4*)(t + kc_row_off(r) + 16 * (2 * s + lh));
 }
 
 // Fragment of a k-strided tile (width W) for the 32 columns starting at c32
@@ -239,11 +256,15 @@ LS_DEV void swap_f32(f32x4 v0, f32x4 v1, f32x4& lo, f32x4& hi) {
 }
 LS_DEV u32x2 pack4(float a, float b, float c, float d) { return u32x2{pack_bf2(a, b), pack_bf2(c, d)}; }
 
-template <bool AK, bool BKC, int EPI, int BM, int BN>
-__global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
-  constexpr int WM = BM / 2, WN = BN / 2;  // wave tile
+template <bool AK, bool BKC, int EPI, int BM, int BN, int NW>
+__global__ __launch_bounds__(NW * 64, 1) void gemm_kernel(GemmArgs p) {
+  // NW waves: 4 (one per SIMD, 2 x 2 wave tiles) or 8 (two per SIMD, 4 x 2)
+  static_assert(NW == 4 || NW == 8, "4 or 8 waves");
+  constexpr int WM = BM / (NW / 2), WN = BN / 2;  // wave tile
+  static_assert(WM % 32 == 0 && WN % 32 == 0, "wave tiles of whole 32 x 32 blocks");
   constexpr int TM = WM / 32, TN = WN / 32;
-  constexpr int NA = AK ? BM / 32 : ks_loads<BM>(), NB = BKC ? BN / 32 : ks_loads<BN>();  // loads per wave and tile
+  constexpr int NA = AK ? BM / (8 * NW) : ks_blocks<BM>() / NW;  // loads per wave and tile
+  constexpr int NB = BKC ? BN / (8 * NW) : ks_blocks<BN>() / NW;
   constexpr int NL = NA + NB;                                    // loads per wave and tile
   constexpr int NMF = TM * TN;                                   // MFMAs per k-step
   constexpr int NRU = TM + TN;                                   // fragments per k-step
@@ -269,10 +290,14 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
   constexpr int BS = KSTEPS - RA;  // the k-step of a tile that holds the barrier
   constexpr bool KSEG = !BKC;  // a k-strided B may come from up to three buffers along k
   constexpr bool GLU = EPI == EPI_GLU_FWD;
-  constexpr uint32_t STAGE_BYTES = 2 * TILE_ELEMS * 2;
+  constexpr uint32_t A_BYTES = AK ? (BM / 8) * KC_PITCH : TILE_ELEMS * 2;
+  constexpr uint32_t B_BYTES = BKC ? (BN / 8) * KC_PITCH : TILE_ELEMS * 2;
+  constexpr uint32_t STAGE_BYTES = A_BYTES + B_BYTES;
+  // the epilogue stages results in the first 128 KB
+  constexpr uint32_t LDS_BYTES = 2 * STAGE_BYTES > 4 * TILE_ELEMS * 2 ? 2 * STAGE_BYTES : 4 * TILE_ELEMS * 2;
   // Two LDS stages of [A tile | B tile].  The buffer->LDS loads are inline
   // assembly the compiler does not see, so the stage can be picked at run time.
-  __shared__ __attribute__((aligned(1024))) bf16_t lds[2][2 * TILE_ELEMS];
+  __shared__ __attribute__((aligned(1024))) char lds[LDS_BYTES];
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -309,25 +334,27 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
   OpLoads<NA> la;
   OpLoads<NB> lb;
   if constexpr (AK) {
-    kc_setup(la, p.A, m0 + wave * NA * 8, p.M, p.lda, lane);
+    kc_setup(la, p.A, m0 + 64 * (wave * NA >> 3), p.M, p.lda, lane, wave * NA);
   } else {
-    ks_setup<NA, BM>(la, m0, p.M, p.lda, wave, lane);
+    ks_setup<NA, BM, NW>(la, m0, p.M, p.lda, wave, lane);
     la.r = rsrc(p.A, clamp_bytes((int64_t)K * p.lda * 2));
   }
   if constexpr (BKC) {
-    const int rb = n0 + wave * NB * 8;  // first row of the wave's blocks (uniform)
+    const int rb = n0 + 64 * (wave * NB >> 3);  // first row of the wave's 64-row segment (uniform)
     if constexpr (GLU) {
-      // gate and up rows interleaved in blocks of 64: a wave's 64 rows are one block
-      kc_setup(lb, (rb >> 6) & 1 ? p.B[1] : p.B[0], (rb >> 7) * 64, p.glu_rows, p.ldb, lane);
+      // gate and up rows interleaved in blocks of 64: a wave's blocks lie in one segment
+      static_assert(BN == 256, "a wave's blocks in one 64-row segment");
+      kc_setup(lb, (rb >> 6) & 1 ? p.B[1] : p.B[0], (rb >> 7) * 64, p.glu_rows, p.ldb, lane, wave * NB);
     } else {
-      // row segments start at multiples of 64, so a wave's 64 rows lie in one
+      // row segments start at multiples of 64; a wave's blocks lie in one of them
+      // when B is split (256-wide tiles), or span two of a single buffer
       const int sg = rb >= p.b_start[2] ? 2 : (rb >= p.b_start[1] ? 1 : 0);
       const int st = sg == 2 ? p.b_start[2] : (sg == 1 ? p.b_start[1] : 0);
       const int en = min(p.N, sg == 2 ? p.N : (sg == 1 ? p.b_start[2] : p.b_start[1]));
-      kc_setup(lb, p.B[sg], rb - st, en - st, p.ldb, lane);
+      kc_setup(lb, p.B[sg], rb - st, en - st, p.ldb, lane, wave * NB);
     }
   } else {
-    ks_setup<NB, BN>(lb, n0, p.N, p.ldb, wave, lane);
+    ks_setup<NB, BN, NW>(lb, n0, p.N, p.ldb, wave, lane);
     if constexpr (!KSEG) lb.r = rsrc(p.B[0], clamp_bytes((int64_t)K * p.ldb * 2));
   }
 
@@ -350,8 +377,10 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
       sob = BKC ? (uint32_t)(k0 * 2) : (uint32_t)((int64_t)k0 * p.ldb * 2);
     }
   };
-  const uint32_t lds0 = lds_offset(&lds[0][0]);
-  const uint32_t ma = lds0 + wave * NA * 1024, mb = lds0 + TILE_ELEMS * 2 + wave * NB * 1024;
+  // The next tile's cursor.
+  auto advance = [&]() { set_cursor(ck + kval); };
+  const uint32_t lds0 = lds_offset(&lds[0]);
+  const uint32_t ma = lds0 + wave * NA * (AK ? KC_PITCH : 1024), mb = lds0 + A_BYTES + wave * NB * (BKC ? KC_PITCH : 1024);
   // Load q of the tile at the cursor (A loads first) into the stage at byte offset stage_off.
   auto issue = [&](int q, uint32_t stage_off) {
     if (q < NA) load_one<AK, NA, BM>(la, q, soa, kval, ma + stage_off, wave);
@@ -370,13 +399,13 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
   u32x4 af[NBUF][TM], bfr[NBUF][TN];
   // Fragment u of a k-step: A fragments 0 .. TM-1, then B fragments.
   auto read_unit = [&](int stage, int s, int buf, int u) {
-    const bf16_t* as = lds[stage];
-    const bf16_t* bs = lds[stage] + TILE_ELEMS;
+    const char* as = lds + stage * STAGE_BYTES;
+    const char* bs = as + A_BYTES;
     if (u < TM) {
-      af[buf][u] = AK ? frag_kc(as, wm * WM + 32 * u + lr, s, lh) : frag_ks<BM>(as, wm * WM + 32 * u, s, lane);
+      af[buf][u] = AK ? frag_kc(as, wm * WM + 32 * u + lr, s, lh) : frag_ks<BM>((const bf16_t*)as, wm * WM + 32 * u, s, lane);
     } else {
       const int v = u - TM;
-      bfr[buf][v] = BKC ? frag_kc(bs, wn * WN + 32 * v + lr, s, lh) : frag_ks<BN>(bs, wn * WN + 32 * v, s, lane);
+      bfr[buf][v] = BKC ? frag_kc(bs, wn * WN + 32 * v + lr, s, lh) : frag_ks<BN>((const bf16_t*)bs, wn * WN + 32 * v, s, lane);
     }
   };
 
@@ -417,12 +446,12 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
           // the later loads of the next tile (its first ones went out in the previous tile)
           if constexpr (NX >= 1 && at >= KSTEPS * NMF && at - KSTEPS * NMF == s * NMF + i) {
             issue(q, there);
-            if constexpr (q == NL - 1) set_cursor(ck + kval);
+            if constexpr (q == NL - 1) advance();
           }
           // the first loads of the tile after next, into this stage
           if constexpr (NX >= 2 && at < KSTEPS * NMF && at == s * NMF + i) {
             issue(q, here);
-            if constexpr (q == NL - 1) set_cursor(ck + kval);
+            if constexpr (q == NL - 1) advance();
           }
         });
         __builtin_amdgcn_sched_barrier(0);
@@ -440,11 +469,11 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
   set_cursor(kbeg);
 #pragma unroll
   for (int q = 0; q < NL; ++q) issue(q, 0);
-  set_cursor(ck + kval);
+  advance();
   if (nk > 1) {
 #pragma unroll
     for (int q = 0; q < FIRST; ++q) issue(q, STAGE_BYTES);
-    if (FIRST == NL) set_cursor(ck + kval);
+    if (FIRST == NL) advance();
     LS_WAIT_VMCNT(FIRST);
   } else {
     LS_WAIT_VMCNT(0);
@@ -470,7 +499,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
   // 512 B, 32 rows) with the 16-byte chunk index XOR-swizzled by the row, so the
   // column-wise writes from the MFMA layout and the row-wise reads both avoid
   // bank conflicts; a 96-wide wave tile uses 12 of the 16 (24 of the 32) chunks.
-  bf16_t* stg = &lds[wave >> 1][(wave & 1) * TILE_ELEMS];  // 32 KB per wave
+  bf16_t* stg = (bf16_t*)lds + wave * (4 * TILE_ELEMS / NW);  // 128 KB / NW per wave
   float* stgf = (float*)stg;
   auto sb = [](int r, int col) { return r * 128 + ((((col >> 3) ^ (r & 15)) << 3) | (col & 7)); };
   auto sf = [](int r, int col) { return r * 128 + ((((col >> 2) ^ (r & 31)) << 2) | (col & 3)); };
@@ -559,7 +588,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
             put4(32 * i + lr, 32 * j + 8 * q + 4 * lh, v);  // [g(64) | u(64)] per row
           }
 #pragma unroll 4
-      for (int t = 0; t < 32; ++t) {
+      for (int t = 0; t < WM / 4; ++t) {
         const int c = lane + 64 * t, r = c >> 4, cc = c & 15;
         const u32x4 v = *(const u32x4*)&stg[sb(r, cc * 8)];
         const int f = (cc & 7) * 8;  // feature offset within the 64
@@ -582,7 +611,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
           put4(32 * i + lr, 32 * j + 8 * q + 4 * lh, v);
         }
 #pragma unroll 4
-    for (int t = 0; t < 16; ++t) {
+    for (int t = 0; t < WM / 8; ++t) {
       const int c = lane + 64 * t, r = c >> 3, cc = c & 7;
       const u32x4 v = *(const u32x4*)&stg[sb(r, cc * 8)];
       if (mw + r < p.M && cc * 8 < nvalid) *(u32x4*)(p.act + (int64_t)(mw + r) * p.glu_I + col0 + cc * 8) = v;
@@ -710,10 +739,20 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(GemmArgs p) {
   }
 }
 
-template <bool AK, bool BKC, int EPI, int BM, int BN>
+// Waves per workgroup, chosen by measurement on the block's products: two per
+// SIMD (8) for the weight-gradient (TN) and plain input-gradient (NN)
+// products, whose k-strided operands are read with transposing LDS reads;
+// one per SIMD (4) for the forward (NT) products and the SwiGLU backward
+// epilogue (which needs the registers).  BM = 192 tiles keep 4 (a wave tile
+// of 48 rows is not whole 32-row blocks).
+template <bool AK, bool BKC, int EPI, int BM>
+constexpr int waves_of() {
+  return BM == 256 && (!AK || (!BKC && EPI == EPI_BF16)) ? 8 : 4;
+}
+template <bool AK, bool BKC, int EPI, int BM, int BN, int NW = waves_of<AK, BKC, EPI, BM>()>
 hipError_t launch(const GemmArgs& a, hipStream_t s) {
   const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_kernel<AK, BKC, EPI, BM, BN>), dim3(tiles * a.ksplit), dim3(NT), 0, s, a);
+  hipLaunchKernelGGL((gemm_kernel<AK, BKC, EPI, BM, BN, NW>), dim3(tiles * a.ksplit), dim3(NW * 64), 0, s, a);
   return hipGetLastError();
 }
 
@@ -810,12 +849,14 @@ hipError_t gemm(const GemmArgs& args, hipStream_t s) {
   if (a.b_kcontig && ((a.b_start[1] % 64 && a.b_start[1] < a.N) || (a.b_start[2] % 64 && a.b_start[2] < a.N)))
     return hipErrorInvalidValue;
   if (a.a_kcontig && a.b_kcontig) {
+    // 192-wide tiles put a wave's B blocks in two 64-row segments: one buffer only
+    const bool n192 = a.b_start[1] >= a.N;
     switch (a.epi) {
       case EPI_BF16:
-        return pick_tile(a.M, a.N, false, true) == 256192 ? launch<true, true, EPI_BF16, 256, 192>(a, s)
+        return pick_tile(a.M, a.N, false, n192) == 256192 ? launch<true, true, EPI_BF16, 256, 192>(a, s)
                                                           : launch<true, true, EPI_BF16, 256, 256>(a, s);
       case EPI_RESID:
-        return pick_tile(a.M, a.N, false, true) == 256192 ? launch<true, true, EPI_RESID, 256, 192>(a, s)
+        return pick_tile(a.M, a.N, false, n192) == 256192 ? launch<true, true, EPI_RESID, 256, 192>(a, s)
                                                           : launch<true, true, EPI_RESID, 256, 256>(a, s);
       case EPI_ROPE:
         return a.head_dim == 64 ? launch<true, true, EPI_ROPE64, 256, 256>(a, s)
