@@ -24,8 +24,7 @@ if ROOT not in sys.path:
 METRIC = "decoder-block fwd+bwd TFLOP/s and MFU (bf16), 3B shape seq 2048, 1 MI355X"  # the default --config 3b
 PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 matrix peak (256 CUs x 4096 FLOP/clk x 2.4 GHz)
 PEAK_HBM_GBS = 8000.0
-DOMINANT = "gate/up projection"  # the largest single kernel launch of the step
-DOMINANT_KERNEL = "gemm_kernel<true, true, 3, 256, 256>"  # its HIP kernel (gate/up product + SwiGLU epilogue)
+STACK_DOMINANT = "gate/up projection"  # the stack's roofline launch: the largest product of each block
 COPY_BYTES = 1 << 30  # size of the plain device copy used to calibrate the HBM byte counters
 
 
@@ -33,24 +32,61 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def dominant_flops(c) -> float:
-    """Algorithmic FLOPs of one gate/up projection launch: [T, H] x [H, 2I]."""
-    return 2.0 * c.tokens * (2 * c.intermediate) * c.hidden
+LAUNCH_DESC = {
+    "qkv projection": "bf16 MFMA GEMM [T,H]x[H,Dq+2Dkv] + fused RoPE",
+    "output projection": "bf16 MFMA GEMM [T,Dq]x[Dq,H] + fused residual",
+    "gate/up projection": "bf16 MFMA GEMM [T,H]x[H,2I] + fused SwiGLU",
+    "down projection": "bf16 MFMA GEMM [T,I]x[I,H] + fused residual",
+    "dact": "bf16 MFMA GEMM [T,H]x[H,I] + fused SwiGLU backward",
+    "dWd": "bf16 MFMA GEMM [H,T]x[T,I], fp32 accumulate",
+    "dh2": "bf16 MFMA GEMM [T,2I]x[2I,H] (input gradient of the gate/up projection)",
+    "dWg/dWu": "bf16 MFMA GEMM [2I,T]x[T,H], fp32 accumulate",
+    "dO": "bf16 MFMA GEMM [T,H]x[H,Dq]",
+    "dWo": "bf16 MFMA GEMM [H,T]x[T,Dq], fp32 accumulate",
+    "dh1": "bf16 MFMA GEMM [T,Dq+2Dkv]x[Dq+2Dkv,H]",
+    "dWqkv": "bf16 MFMA GEMM [Dq+2Dkv,T]x[T,H], fp32 accumulate",
+    "attention fwd": "causal GQA flash attention forward (bf16 MFMA)",
+    "attention bwd": "causal GQA flash attention backward (bf16 MFMA)",
+}
 
 
-def dominant_traffic():
-    """HBM bytes per launch of the dominant kernel from the committed counter
-    runs, or None when the kernel sources changed since they were taken."""
+def traffic_key(label: str, config: str) -> str:
+    return f"{label.replace('/', '_').replace(' ', '_')}_{config}"
+
+
+def launch_traffic(label: str, config: str):
+    """HBM bytes per launch of a labelled launch from the committed counter
+    runs, or None when there are none or the kernel sources changed since."""
     from paper_2510_02483_amd import profiling
 
     path = profiling.TRAFFIC_JSON
     if not os.path.exists(path):
         return None
     with open(path) as f:
-        entry = json.load(f).get("gate_up_3b")
+        entry = json.load(f).get(traffic_key(label, config))
     if not entry or entry.get("sources_hash") != profiling.sources_hash():
         return None
     return entry["traffic_bytes"]
+
+
+def launch_breakdown(step_fn, labels, steps: int):
+    """Mean duration (ms) and launches per step of every labelled launch,
+    from HIP events the library records around it, over `steps` untimed steps
+    per label."""
+    import torch
+
+    from paper_2510_02483_amd import lib
+
+    out = {}
+    for label in labels:
+        lib.ls_timing_begin(label, 8 * steps)
+        for _ in range(steps):
+            step_fn()
+        torch.cuda.synchronize()
+        n, ms = lib.ls_timing_end()
+        if n:
+            out[label] = (n // steps, ms)
+    return out
 
 
 def calibrate_copy(iters: int = 5):
@@ -129,13 +165,17 @@ def kernel_only(args):
         torch.cuda.synchronize()
         return start.elapsed_time(stop) / n
 
-    if args.kernel == "gemm_nt":
+    if args.kernel in ("gemm_nt", "torch_nt"):
         M, N, K = (int(v) for v in args.shape.split(","))
         A = torch.randn(M, K, generator=g).to(torch.bfloat16).cuda()
         B = torch.randn(N, K, generator=g).to(torch.bfloat16).cuda()
         C = torch.empty(M, N, dtype=torch.bfloat16, device="cuda")
-        ms = timed(lambda: lib.ls_gemm_nt(A, B, C), args.steps)
-        out = {"kernel": "gemm_nt", "shape": [M, N, K], "ms": round(ms, 4),
+        if args.kernel == "gemm_nt":
+            fn = lambda: lib.ls_gemm_nt(A, B, C)  # noqa: E731
+        else:  # yardstick only: the vendor library's product of the same shape, timed, never part of the path
+            fn = lambda: torch.mm(A, B.t(), out=C)  # noqa: E731
+        ms = timed(fn, args.steps)
+        out = {"kernel": args.kernel, "shape": [M, N, K], "ms": round(ms, 4),
                "tflops": round(2.0 * M * N * K / (ms * 1e-3) / 1e12, 2)}
     else:
         c = configs.PRESETS[args.config]
@@ -197,7 +237,7 @@ def stack_bench(args):
     stream = torch.cuda.current_stream()
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     per_step = sc.n_layers * (2 if sc.recompute else 1)
-    lib.ls_timing_begin(DOMINANT, args.steps * per_step)
+    lib.ls_timing_begin(STACK_DOMINANT, args.steps * per_step)
     torch.cuda.synchronize()
     start.record(stream)
     for _ in range(args.steps):
@@ -219,7 +259,7 @@ def stack_bench(args):
     energy = energy_of(lambda: st.step(accumulate=True), sc.tokens, args)
     fl = flops.stack_fwd_bwd_flops(sc)
     tflops = fl / (ms * 1e-3) / 1e12
-    dom_tflops = dominant_flops(sc.block) / (dom_ms * 1e-3) / 1e12 if n_dom else None
+    dom_tflops = flops.launch_flops(sc.block)[STACK_DOMINANT] / (dom_ms * 1e-3) / 1e12 if n_dom else None
     c = sc.block
     result = {
         "metric": f"model fwd+bwd TFLOP/s and MFU (bf16), {sc.name} ({sc.n_layers} blocks), 1 MI355X",
@@ -254,7 +294,7 @@ def stack_bench(args):
                       "frac": round(ADAMW_BYTES_PER_PARAM * st.n_params / (opt_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)},
         "energy": energy,
         "roofline": {
-            "kernel": f"{DOMINANT} (bf16 MFMA GEMM [T,H]x[H,2I] + fused SwiGLU)",
+            "kernel": f"{STACK_DOMINANT} ({LAUNCH_DESC[STACK_DOMINANT]})",
             "bound": "mfma",
             "achieved": round(dom_tflops, 2) if dom_tflops else None,
             "peak": PEAK_BF16_TFLOPS,
@@ -278,8 +318,9 @@ def main():
     ap.add_argument("--cpu-sequences", type=int, default=4, help="sequences in the oracle's timed sample")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run only a plain 1 GiB device copy (for counter calibration) and exit")
-    ap.add_argument("--kernel", choices=("gemm_nt", "attention"),
-                    help="time one kernel family instead of the block step (for per-kernel counters)")
+    ap.add_argument("--kernel", choices=("gemm_nt", "torch_nt", "attention"),
+                    help="time one kernel family instead of the block step (for per-kernel counters); torch_nt: "
+                         "the vendor library's product of the same shape through torch, as a yardstick")
     ap.add_argument("--shape", default="8192,16384,3072", help="M,N,K of --kernel gemm_nt")
     ap.add_argument("--energy-seconds", type=float, default=2.0,
                     help="seconds of extra steps read against the GPU energy counter (0: skip)")
@@ -318,9 +359,16 @@ def main():
         blk.step(accumulate=True)
     torch.cuda.synchronize()
 
+    # untimed: every labelled launch's duration; the roofline launch is the one
+    # that takes the largest share of the step
+    lfl = flops.launch_flops(c)
+    breakdown = launch_breakdown(lambda: blk.step(accumulate=True), flops.BLOCK_LAUNCHES, max(2, args.warmup))
+    dominant = max((lb for lb in breakdown if lb in lfl), key=lambda lb: breakdown[lb][0] * breakdown[lb][1])
+    per_step = breakdown[dominant][0]
+
     stream = torch.cuda.current_stream()
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    lib.ls_timing_begin(DOMINANT, args.steps)
+    lib.ls_timing_begin(dominant, args.steps * per_step)
     torch.cuda.synchronize()
     start.record(stream)
     for _ in range(args.steps):
@@ -333,7 +381,14 @@ def main():
     energy = energy_of(lambda: blk.step(accumulate=True), c.tokens, args)
     fl = flops.block_fwd_bwd_flops(c)
     tflops = fl / (ms * 1e-3) / 1e12
-    dom_tflops = dominant_flops(c) / (dom_ms * 1e-3) / 1e12 if n_dom else None
+    dom_tflops = lfl[dominant] / (dom_ms * 1e-3) / 1e12 if n_dom else None
+    launches = {}
+    for lb, (n, lms) in breakdown.items():
+        e = {"per_step": n, "us": round(lms * 1e3, 1)}
+        if lb in lfl:
+            tf = lfl[lb] / (lms * 1e-3) / 1e12
+            e.update(tflops=round(tf, 1), frac=round(tf / PEAK_BF16_TFLOPS, 4))
+        launches[lb] = e
     result = {
         "metric": METRIC if args.config == "3b" else f"decoder-block fwd+bwd TFLOP/s and MFU (bf16), {c.name}, 1 MI355X",
         "value": round(tflops, 2),
@@ -357,16 +412,18 @@ def main():
         "tflops_noncausal_convention": round(flops.block_fwd_bwd_flops(c, causal=False) / (ms * 1e-3) / 1e12, 2),
         "energy": energy,
         "roofline": {
-            "kernel": f"{DOMINANT} (bf16 MFMA GEMM [T,H]x[H,2I] + fused SwiGLU)",
+            "kernel": f"{dominant} ({LAUNCH_DESC.get(dominant, dominant)}): the launch with the largest share of the step",
             "bound": "mfma",
             "achieved": round(dom_tflops, 2) if dom_tflops else None,
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(dom_tflops / PEAK_BF16_TFLOPS, 4) if dom_tflops else None,
-            "traffic": dominant_traffic() if args.config == "3b" else None,
+            "traffic": launch_traffic(dominant, c.name),
             "launches": n_dom,
             "mean_ms": round(dom_ms, 4),
+            "flops_per_launch": lfl[dominant],
         },
+        "launches": launches,
     }
     if not args.no_cpu_baseline and args.config == "3b":
         log("timing the fp64 oracle on a sample of the workload ...")

@@ -57,3 +57,24 @@ def stack_fwd_bwd_flops(sc: StackConfig, causal: bool = True) -> float:
     the tied LM head (recomputation in the backward pass is not counted)."""
     return sc.n_layers * block_fwd_bwd_flops(sc.block, causal) + \
         lm_head_fwd_bwd_flops(sc.tokens, sc.block.hidden, sc.vocab)
+
+
+# Labelled launches of one block step (forward, then the MLP and attention
+# backward passes) in the order the library issues them.
+BLOCK_LAUNCHES = ("rmsnorm fwd", "qkv projection", "attention fwd", "output projection", "gate/up projection",
+                  "down projection", "dact", "dWd", "dh2", "dWg/dWu", "rmsnorm bwd", "dO", "dWo", "attention bwd",
+                  "dh1", "dWqkv")
+
+
+def launch_flops(cfg: BlockConfig) -> dict:
+    """Model FLOPs of each labelled matrix-product and attention launch of one
+    block step (2 M N K per product; attention backward = 2 x forward).  The
+    RMSNorm launches are bandwidth-bound and carry no entry."""
+    T, H, I, dq, dkv = cfg.tokens, cfg.hidden, cfg.intermediate, cfg.dq, cfg.dkv
+    dqkv = dq + 2 * dkv
+    att = attention_fwd_flops(cfg)
+    return {"qkv projection": 2.0 * T * dqkv * H, "attention fwd": att, "output projection": 2.0 * T * H * dq,
+            "gate/up projection": 2.0 * T * 2 * I * H, "down projection": 2.0 * T * H * I,
+            "dact": 2.0 * T * I * H, "dWd": 2.0 * T * H * I, "dh2": 2.0 * T * 2 * I * H,
+            "dWg/dWu": 2.0 * T * 2 * I * H, "dO": 2.0 * T * dq * H, "dWo": 2.0 * T * H * dq,
+            "attention bwd": 2.0 * att, "dh1": 2.0 * T * dqkv * H, "dWqkv": 2.0 * T * dqkv * H}

@@ -51,3 +51,35 @@ def test_block_flops_direct_count():
 
 def test_3b_block_total():
     assert abs(block_fwd_bwd_flops(configs.B3) / 1e12 - 5.2572) < 1e-3
+
+
+def test_launch_flops_sum_to_the_block():
+    """The labelled launches of a block step carry all of its model FLOPs."""
+    from paper_2510_02483_amd import configs, flops
+    for c in (configs.B3, configs.TINY, configs.B30, configs.PAPER_3B):
+        lf = flops.launch_flops(c)
+        assert set(lf) <= set(flops.BLOCK_LAUNCHES)
+        assert abs(sum(lf.values()) - flops.block_fwd_bwd_flops(c)) < 1e-6 * flops.block_fwd_bwd_flops(c)
+    lf = flops.launch_flops(configs.B3)
+    # the three 0.82-TFLOP products of the MLP
+    assert lf["gate/up projection"] == lf["dh2"] == lf["dWg/dWu"] == 2.0 * 8192 * 16384 * 3072
+
+
+def test_profile_launch_labelling():
+    """Dispatches of block steps are named after their launches by position,
+    split-K reductions joining their product, set-up kernels left out."""
+    from paper_2510_02483_amd import profiling
+    g = "gemm_kernel<...>"
+    step = (["rmsnorm_fwd_kernel<6>", "rope_table_kernel", g, "attn_fwd_kernel<128>", g, "rmsnorm_fwd_kernel<6>", g, g,
+             g, g, "kpart_reduce_kernel", g, g, "rmsnorm_bwd_kernel<6>", "column_sum_kernel", "rope_table_kernel", g, g,
+             "attn_bwd_pre_kernel<128>", "attn_bwd_dkdv_kernel<128, true>", "attn_bwd_dkdv_reduce<128>",
+             "attn_bwd_dq_kernel<128>", g, g, "rmsnorm_bwd_kernel<6>", "column_sum_kernel"])
+    names = ["FillFunctor"] + step + step + ["copyBuffer"]
+    steps = profiling.label_steps(names)
+    assert len(steps) == 2
+    labels = [lab for _, lab in steps[0]]
+    assert labels[2] == "qkv projection" and labels[3] == "attention fwd"
+    assert labels[9:11] == ["dWd", "dWd"]  # the split-K reduction belongs to its product
+    assert labels.count("attention bwd") == 4 and labels.count("rmsnorm bwd") == 4
+    assert [lab for lab in labels if lab in profiling.GEMM_ORDER][-1] == "dWqkv"
+    assert steps[1][0][0] == 1 + len(step)
