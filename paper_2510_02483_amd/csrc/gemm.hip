@@ -625,7 +625,10 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_kernel(GemmArgs p) {
     // values have arrived when it is processed.
     bf16_t* sg_ = stg;             // gate / dg rows (32 x 128)
     bf16_t* su_ = stg + 32 * 128;  // up / du rows
-    u32x4 gpre[2][8], upre[2][8];
+    // (two blocks in flight with one wave per SIMD; one with two, whose
+    // registers are half as many)
+    constexpr int PF = NW == 8 ? 1 : 2;
+    u32x4 gpre[PF][8], upre[PF][8];
     auto fetch = [&](int i, int b) {
       const int mb = mw + 32 * i;
 #pragma unroll
@@ -642,17 +645,17 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_kernel(GemmArgs p) {
       }
     };
     fetch(0, 0);
-    if constexpr (TM > 1) fetch(1, 1);
+    if constexpr (TM > 1 && PF > 1) fetch(1, 1);
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
       const int mb = mw + 32 * i;
 #pragma unroll
       for (int t = 0; t < 8; ++t) {
         const int c = lane + 64 * t, r = c >> 4, cc = c & 15;
-        *(u32x4*)&sg_[sb(r, cc * 8)] = gpre[i & 1][t];
-        *(u32x4*)&su_[sb(r, cc * 8)] = upre[i & 1][t];
+        *(u32x4*)&sg_[sb(r, cc * 8)] = gpre[i % PF][t];
+        *(u32x4*)&su_[sb(r, cc * 8)] = upre[i % PF][t];
       }
-      if (i + 2 < TM) fetch(i + 2, i & 1);
+      if (i + PF < TM) fetch(i + PF, i % PF);
 #pragma unroll
       for (int j = 0; j < TN; ++j)
 #pragma unroll
@@ -740,14 +743,14 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_kernel(GemmArgs p) {
 }
 
 // Waves per workgroup, chosen by measurement on the block's products: two per
-// SIMD (8) for the weight-gradient (TN) and plain input-gradient (NN)
-// products, whose k-strided operands are read with transposing LDS reads;
-// one per SIMD (4) for the forward (NT) products and the SwiGLU backward
-// epilogue (which needs the registers).  BM = 192 tiles keep 4 (a wave tile
-// of 48 rows is not whole 32-row blocks).
+// SIMD (8) for the weight-gradient (TN) and input-gradient (NN) products,
+// whose k-strided operands are read with transposing LDS reads (the SwiGLU
+// backward epilogue then prefetches one 32-row block of the saved gate/up
+// values instead of two); one per SIMD (4) for the forward (NT) products.
+// BM = 192 tiles keep 4 (a wave tile of 48 rows is not whole 32-row blocks).
 template <bool AK, bool BKC, int EPI, int BM>
 constexpr int waves_of() {
-  return BM == 256 && (!AK || (!BKC && EPI == EPI_BF16)) ? 8 : 4;
+  return BM == 256 && (!AK || (!BKC && (EPI == EPI_BF16 || EPI == EPI_GLU_BWD))) ? 8 : 4;
 }
 template <bool AK, bool BKC, int EPI, int BM, int BN, int NW = waves_of<AK, BKC, EPI, BM>()>
 hipError_t launch(const GemmArgs& a, hipStream_t s) {
