@@ -191,19 +191,42 @@ LS_DEV QTile q_tile(const AttnShape& sh) {
   return QTile{nqt - 1 - x / per, (x % per) % sh.nq, (x % per) / sh.nq};
 }
 
+// The two halves of a wave (lanes 0-31 and 32-63) hold the same 32 queries
+// at different keys: combine a per-lane value with the other half's, through a
+// lane swap on the vector unit rather than an LDS permute (which would also
+// wait for every LDS read in flight).
+LS_DEV float halves_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+LS_DEV float halves_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// Online softmax with a lagging reference maximum: the running reference m
+// moves only when some query's scores exceed it by more than 2^LAG (base 2), so
+// that most tiles skip the rescale of O and l.  P = 2^(s - m) then lies in
+// (0, 2^LAG]: bf16 keeps its relative precision at any such magnitude, and O,
+// l in fp32 stay far from overflow.  The result, O = sum P V / sum P and the
+// log-sum-exp m + log2 l, does not depend on the reference point.
+constexpr float LAG = 8.0f;
+
 template <int D>
 __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnShape sh, const bf16_t* __restrict__ qkv,
                                                            bf16_t* __restrict__ o, float* __restrict__ lse,
                                                            float sl2) {
   __shared__ __attribute__((aligned(1024))) bf16_t Ks[2][BKV * D];
   __shared__ __attribute__((aligned(1024))) bf16_t Vs[2][BKV * D];
+  // the scale in a register before the loop: a scalar load still in flight
+  // at the loop entry makes the first LDS wait of every tile a full wait
+  asm volatile("" : "+s"(sl2));
 
   const int S = sh.seq, nq = sh.nq, nkv = sh.nkv;
   const QTile qtile = q_tile(sh);
   const int h = qtile.h, b = qtile.b, kvh = h / (nq / nkv);
   const int64_t ld = (int64_t)(nq + 2 * nkv) * D;
   const bf16_t* base = qkv + (int64_t)b * S * ld;
-  const i32x4 rs = rsrc(base, clamp_bytes((int64_t)S * ld * 2));
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, lr = lane & 31, lh = lane >> 5;
   const int q0 = qtile.qt * BQ;
   const int qrow = q0 + 32 * wave + lr;
@@ -212,8 +235,35 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnShape sh, const bf
 
   const int kv_end = min(S, q0 + BQ);
   const int nkt = (kv_end + BKV - 1) / BKV;
-  load_tile<D, BKV>(rs, ld, 0, S, kcol, Ks[0], wave, lane);
-  load_tile<D, BKV>(rs, ld, 0, S, vcol, Vs[0], wave, lane);
+
+  // This wave's share of a key tile, as per-lane byte offsets from the tile's
+  // first row at the K columns (the same rows and swizzle as load_tile); they
+  // are the same for every tile and, with the resource moved to the V
+  // columns, for V.  A tile's resource starts at its first row and ends at row
+  // S, so rows past the sequence read zero.
+  constexpr int CPR = D / 8, RPI = 64 / CPR, PER = BKV / RPI / 4;
+  uint32_t toff[PER];
+#pragma unroll
+  for (int jj = 0; jj < PER; ++jj) {
+    const int rr = (wave * PER + jj) * RPI + lane / CPR;
+    const int c = (lane % CPR) ^ tile_swz<D>(rr);
+    toff[jj] = ((uint32_t)rr * (uint32_t)ld + (uint32_t)(kcol + 8 * c)) * 2u;
+  }
+  const int64_t vshift = (int64_t)(vcol - kcol) * 2;
+  auto load_kv = [&](int kv0, bf16_t* kt, bf16_t* vt) {
+    const int64_t rest = (int64_t)(S - kv0) * ld * 2;
+    const char* t0 = (const char*)(base + (int64_t)kv0 * ld);
+    DmaLoad l[PER];
+    const i32x4 rk = rsrc(t0, clamp_bytes(rest));
+#pragma unroll
+    for (int jj = 0; jj < PER; ++jj) l[jj] = DmaLoad{rk, toff[jj]};
+    dma16_group<PER>(l, kt + wave * PER * 512);
+    const i32x4 rv = rsrc(t0 + vshift, clamp_bytes(rest - vshift));
+#pragma unroll
+    for (int jj = 0; jj < PER; ++jj) l[jj] = DmaLoad{rv, toff[jj]};
+    dma16_group<PER>(l, vt + wave * PER * 512);
+  };
+  load_kv(0, Ks[0], Vs[0]);
 
   u32x4 qf[D / 16];
 #pragma unroll
@@ -238,10 +288,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnShape sh, const bf
   auto step = [&](auto cur_c, int kt) {
     constexpr int cur = decltype(cur_c)::value;
     const int kv0 = kt * BKV;
-    if (kt + 1 < nkt) {
-      load_tile<D, BKV>(rs, ld, kv0 + BKV, S, kcol, Ks[cur ^ 1], wave, lane);
-      load_tile<D, BKV>(rs, ld, kv0 + BKV, S, vcol, Vs[cur ^ 1], wave, lane);
-    }
+    if (kt + 1 < nkt) load_kv(kv0 + BKV, Ks[cur ^ 1], Vs[cur ^ 1]);
     if (kv0 <= wave_qmax) {  // else every key of the tile is in this wave's future
       f32x16 sacc[BKV / 32];
 #pragma unroll
@@ -266,25 +313,25 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnShape sh, const bf
       for (int bb = 0; bb < BKV / 32; ++bb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[bb][r]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float mnew = fmaxf(m, mx * sl2);  // key 0 is visible to every query: finite from the first tile on
-      const float alpha = ex2(m - mnew);
+      // key 0 is visible to every query: finite from the first tile on
+      const float mc = fmaxf(m, halves_max(mx) * sl2);
+      if (__builtin_amdgcn_ballot_w64(mc > m + LAG)) {
+        const float alpha = ex2(m - mc);
+        m = mc;
+        l *= alpha;
+#pragma unroll
+        for (int i = 0; i < D / 32; ++i) oacc[i] *= alpha;
+      }
       float ls = 0.f;
 #pragma unroll
       for (int bb = 0; bb < BKV / 32; ++bb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float p = ex2(fmaf(sacc[bb][r], sl2, -mnew));
+          const float p = ex2(fmaf(sacc[bb][r], sl2, -m));
           sacc[bb][r] = p;
           ls += p;
         }
-      ls += __shfl_xor(ls, 32);
-      l = l * alpha + ls;
-      m = mnew;
-      if (__builtin_amdgcn_ballot_w64(alpha != 1.0f)) {
-#pragma unroll
-        for (int i = 0; i < D / 32; ++i) oacc[i] *= alpha;
-      }
+      l += halves_sum(ls);
 #pragma unroll
       for (int s = 0; s < BKV / 16; ++s) {
         const u32x4 pf = pack_frag(sacc[s >> 1], 8 * (s & 1));
