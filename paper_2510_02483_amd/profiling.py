@@ -203,7 +203,7 @@ def counters(a):
         lines.append(f"   derived: mean L1->L2 read latency {mean['TCP_TCC_READ_REQ_LATENCY_sum'] / mean['TCP_TCC_READ_REQ_sum']:.0f} cycles")
     if "TCC_HIT_sum" in mean and "TCC_MISS_sum" in mean:
         lines.append(f"   derived: L2 hit rate {100 * mean['TCC_HIT_sum'] / (mean['TCC_HIT_sum'] + mean['TCC_MISS_sum']):.1f}%")
-    if "SQ_INSTS_VALU" in mean and "SQ_INSTS_MFMA" in mean:
+    if "SQ_INSTS_VALU" in mean and mean.get("SQ_INSTS_MFMA", 0) > 0:
         lines.append(f"   derived: non-MFMA VALU instructions per MFMA {(mean['SQ_INSTS_VALU'] - mean['SQ_INSTS_MFMA']) / mean['SQ_INSTS_MFMA']:.2f}")
     with open(a.out, "w") as f:
         f.write("\n".join(lines) + "\n")
