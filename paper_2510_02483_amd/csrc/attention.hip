@@ -76,32 +76,36 @@ LS_DEV int tile_swz(int r) {
   else return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
 }
 
-// Load rows row0 .. row0+ROWS-1, columns col0 .. col0+D-1 of a row-major bf16
-// matrix (leading dimension ld elements, `rows` rows, covered by the buffer
-// resource r) into an LDS tile; rows at or past `rows` read as zero.  Each
-// load fills 1 KB of the tile (64/(D/8) rows); wave w fills the consecutive
-// blocks w*PER .. w*PER+PER-1 with one M0 write.
-// With REMAT the per-lane offsets are recomputed at every call from the lane
-// index (itself recomputed here) rather than hoisted out of the tile loop,
-// where they would hold registers for the whole loop.
-template <int D, int ROWS, bool REMAT = false>
-LS_DEV void load_tile(i32x4 r, int64_t ld, int row0, int rows, int col0, bf16_t* t, int wave, int lane) {
-  constexpr int CPR = D / 8, RPI = 64 / CPR, NI = ROWS / RPI, PER = NI / 4;
-  static_assert(NI % 4 == 0 && (PER == 2 || PER == 4), "loads split evenly over 4 waves in groups of 2 or 4");
-  if constexpr (REMAT) asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(lane));
-  DmaLoad l[PER];
+// Loads of tiles: rows row0 .. row0+ROWS-1, columns col0 .. col0+D-1 of a
+// row-major bf16 matrix (leading dimension ld elements, `rows` rows) into an
+// LDS tile in the swizzled layout above; rows at or past `rows` read as zero.
+// Each load fills 1 KB of the tile (64/(D/8) rows); wave w fills the
+// consecutive blocks w*PER .. w*PER+PER-1 with one M0 write.  The per-lane
+// byte offsets of the wave's share are computed once, for every tile of a
+// loop; a tile only moves the scalar resource, whose base is the tile's first
+// element and whose end is row `rows` (the tile's columns lie within a row:
+// col0 + D <= ld).
+template <int D, int ROWS>
+struct TileLoader {
+  static constexpr int CPR = D / 8, RPI = 64 / CPR, PER = ROWS / RPI / 4;
+  static_assert(PER == 2 || PER == 4, "loads split evenly over 4 waves in groups of 2 or 4");
+  uint32_t off[PER];
+  LS_DEV TileLoader(int64_t ld, int wave, int lane) {
 #pragma unroll
-  for (int jj = 0; jj < PER; ++jj) {
-    const int j = wave * PER + jj;
-    const int rr = j * RPI + lane / CPR;
-    const int c = (lane % CPR) ^ tile_swz<D>(rr);
-    const int gr = row0 + rr;
-    // 32-bit offsets: every buffer is below 2 GiB
-    const uint32_t off = ((uint32_t)gr * (uint32_t)ld + (uint32_t)(col0 + 8 * c)) * 2u;
-    l[jj] = DmaLoad{r, gr < rows ? off : LS_OOB};
+    for (int jj = 0; jj < PER; ++jj) {
+      const int rr = (wave * PER + jj) * RPI + lane / CPR;
+      const int c = (lane % CPR) ^ tile_swz<D>(rr);
+      off[jj] = ((uint32_t)rr * (uint32_t)ld + (uint32_t)(8 * c)) * 2u;
+    }
   }
-  dma16_group<PER>(l, t + wave * PER * 512);
-}
+  LS_DEV void operator()(const bf16_t* m, int64_t ld, int row0, int rows, int col0, bf16_t* t, int wave) const {
+    const i32x4 r = rsrc(m + (int64_t)row0 * ld + col0, clamp_bytes((int64_t)(rows - row0) * ld * 2 - (int64_t)col0 * 2));
+    DmaLoad l[PER];
+#pragma unroll
+    for (int jj = 0; jj < PER; ++jj) l[jj] = DmaLoad{r, off[jj]};
+    dma16_group<PER>(l, t + wave * PER * 512);
+  }
+};
 
 // 64 floats v[i0 .. i0+63] of a buffer of `n` floats (resource r; entries at or
 // past n read as zero) into t[0..63]; t must hold 256 floats (lanes 16..63 of
@@ -236,32 +240,10 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnShape sh, const bf
   const int kv_end = min(S, q0 + BQ);
   const int nkt = (kv_end + BKV - 1) / BKV;
 
-  // This wave's share of a key tile, as per-lane byte offsets from the tile's
-  // first row at the K columns (the same rows and swizzle as load_tile); they
-  // are the same for every tile and, with the resource moved to the V
-  // columns, for V.  A tile's resource starts at its first row and ends at row
-  // S, so rows past the sequence read zero.
-  constexpr int CPR = D / 8, RPI = 64 / CPR, PER = BKV / RPI / 4;
-  uint32_t toff[PER];
-#pragma unroll
-  for (int jj = 0; jj < PER; ++jj) {
-    const int rr = (wave * PER + jj) * RPI + lane / CPR;
-    const int c = (lane % CPR) ^ tile_swz<D>(rr);
-    toff[jj] = ((uint32_t)rr * (uint32_t)ld + (uint32_t)(kcol + 8 * c)) * 2u;
-  }
-  const int64_t vshift = (int64_t)(vcol - kcol) * 2;
+  const TileLoader<D, BKV> tl(ld, wave, lane);
   auto load_kv = [&](int kv0, bf16_t* kt, bf16_t* vt) {
-    const int64_t rest = (int64_t)(S - kv0) * ld * 2;
-    const char* t0 = (const char*)(base + (int64_t)kv0 * ld);
-    DmaLoad l[PER];
-    const i32x4 rk = rsrc(t0, clamp_bytes(rest));
-#pragma unroll
-    for (int jj = 0; jj < PER; ++jj) l[jj] = DmaLoad{rk, toff[jj]};
-    dma16_group<PER>(l, kt + wave * PER * 512);
-    const i32x4 rv = rsrc(t0 + vshift, clamp_bytes(rest - vshift));
-#pragma unroll
-    for (int jj = 0; jj < PER; ++jj) l[jj] = DmaLoad{rv, toff[jj]};
-    dma16_group<PER>(l, vt + wave * PER * 512);
+    tl(base, ld, kv0, S, kcol, kt, wave);
+    tl(base, ld, kv0, S, vcol, vt, wave);
   };
   load_kv(0, Ks[0], Vs[0]);
 
@@ -483,8 +465,6 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnShape sh, con
   const int64_t ldo = (int64_t)nq * D;
   const bf16_t* base = qkv + (int64_t)b * S * ld;
   const bf16_t* dbase = dout + (int64_t)b * S * ldo;
-  const i32x4 rq_ = rsrc(base, clamp_bytes((int64_t)S * ld * 2));
-  const i32x4 rdo = rsrc(dbase, clamp_bytes((int64_t)S * ldo * 2));
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lr = lane & 31, lh = lane >> 5;
   const int kv0 = kvt * BWD_BKV;
@@ -494,10 +474,11 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(AttnShape sh, con
   const int q_begin = kv0;  // earlier queries see none of these keys
   const int nqt = (S - q_begin + BWD_BQ - 1) / BWD_BQ;
   const int ntiles = Gs * nqt;
+  const TileLoader<D, BWD_BQ> tlq(ld, wave, lane), tlo(ldo, wave, lane);
   auto issue = [&](int t, int st) {
     const int h = kvh * G + hs * Gs + t / nqt, q0 = q_begin + (t % nqt) * BWD_BQ;
-    load_tile<D, BWD_BQ, true>(rq_, ld, q0, S, h * D, stg[st].q, wave, lane);
-    load_tile<D, BWD_BQ, true>(rdo, ldo, q0, S, h * D, stg[st].o, wave, lane);
+    tlq(base, ld, q0, S, h * D, stg[st].q, wave);
+    tlo(dbase, ldo, q0, S, h * D, stg[st].o, wave);
     if (wave == 0) load_vec64(rsrc(lse2 + ((int64_t)b * nq + h) * S, (uint32_t)S * 4), q0, S, stg[st].l, lane);
     if (wave == 1) load_vec64(rsrc(Dv + ((int64_t)b * nq + h) * S, (uint32_t)S * 4), q0, S, stg[st].d, lane);
   };
@@ -729,7 +710,6 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(AttnShape sh, const
   const int64_t ld = (int64_t)(nq + 2 * nkv) * D;
   const int64_t ldo = (int64_t)nq * D;
   const bf16_t* base = qkv + (int64_t)b * S * ld;
-  const i32x4 rs = rsrc(base, clamp_bytes((int64_t)S * ld * 2));
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lr = lane & 31, lh = lane >> 5;
   const int q0 = qtile.qt * BQ;
@@ -739,8 +719,9 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(AttnShape sh, const
 
   const int kv_end = min(S, q0 + BQ);
   const int nkt = (kv_end + BKV - 1) / BKV;
-  load_tile<D, BKV, true>(rs, ld, 0, S, kcol, Ks[0], wave, lane);
-  load_tile<D, BKV, true>(rs, ld, 0, S, vcol, Vs[0], wave, lane);
+  const TileLoader<D, BKV> tl(ld, wave, lane);
+  tl(base, ld, 0, S, kcol, Ks[0], wave);
+  tl(base, ld, 0, S, vcol, Vs[0], wave);
 
   u32x4 qf[NSD], df[NSD];
 #pragma unroll
@@ -796,8 +777,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(AttnShape sh, const
     constexpr int cur = decltype(cur_c)::value;
     const int kv0 = kt * BKV;
     if (kt + 1 < nkt) {
-      load_tile<D, BKV, true>(rs, ld, kv0 + BKV, S, kcol, Ks[cur ^ 1], wave, lane);
-      load_tile<D, BKV, true>(rs, ld, kv0 + BKV, S, vcol, Vs[cur ^ 1], wave, lane);
+      tl(base, ld, kv0 + BKV, S, kcol, Ks[cur ^ 1], wave);
+      tl(base, ld, kv0 + BKV, S, vcol, Vs[cur ^ 1], wave);
     }
     const int hi = qrow - kv0 - 4 * lh;
     static_for<RA>([&](auto j_c) { ring[decltype(j_c)::value] = operand(j_c, cur_c); });
