@@ -214,8 +214,9 @@ def energy_of(step_fn, tokens_per_step: int, args):
         step_fn()
         torch.cuda.synchronize()
 
-    calls, secs, joules = meter.measure(one, args.energy_seconds)
+    calls, secs, joules, sclk = meter.measure(one, args.energy_seconds)
     out = energy.report(calls, secs, joules, tokens_per_step)
+    out["sclk_mhz"] = sclk  # mean shader clock over the same loop
     if meter.error:
         out["error"] = meter.error
     return out
@@ -379,6 +380,7 @@ def main():
     ms = start.elapsed_time(stop) / args.steps
 
     energy = energy_of(lambda: blk.step(accumulate=True), c.tokens, args)
+    sclk = energy.get("sclk_mhz") if energy else None
     fl = flops.block_fwd_bwd_flops(c)
     tflops = fl / (ms * 1e-3) / 1e12
     dom_tflops = lfl[dominant] / (dom_ms * 1e-3) / 1e12 if n_dom else None
@@ -422,6 +424,10 @@ def main():
             "launches": n_dom,
             "mean_ms": round(dom_ms, 4),
             "flops_per_launch": lfl[dominant],
+            # the shader clock measured over the energy loop (same steps, right
+            # after the timed ones) and the peak at that clock
+            "sclk_mhz": sclk,
+            "peak_at_sclk": round(PEAK_BF16_TFLOPS * sclk / 2400.0, 1) if sclk else None,
         },
         "launches": launches,
     }

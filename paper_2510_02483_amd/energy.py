@@ -56,11 +56,40 @@ class EnergyMeter:
         e = self._smi.amdsmi_get_energy_count(self.handle)
         return e["energy_accumulator"] * e["counter_resolution"] * 1e-6
 
+    def gfx_clocks(self):
+        """Current shader clock of each XCD in MHz (the firmware's metrics
+        table), or None when it cannot be read."""
+        if self.handle is None:
+            return None
+        try:
+            m = self._smi.amdsmi_get_gpu_metrics_info(self.handle)
+        except Exception:  # noqa: BLE001
+            return None
+        v = m.get("current_gfxclks")
+        if not isinstance(v, (list, tuple)):
+            v = [m.get("current_gfxclk")]
+        return v
+
     def measure(self, fn, min_seconds: float = 2.0):
         """Run fn() (which must synchronise the device at its end) repeatedly
-        for at least min_seconds; return (calls, seconds, joules or None)."""
+        for at least min_seconds; return (calls, seconds, joules or None,
+        mean shader clock in MHz or None).  The clock is sampled every 10 ms
+        by a second thread while the loop runs."""
+        import threading
+
+        samples, stop = [], threading.Event()
+
+        def sample():
+            while not stop.wait(0.01):
+                c = self.gfx_clocks()
+                if c is not None:
+                    samples.append(c)
+
+        th = threading.Thread(target=sample, daemon=True) if self.handle is not None else None
         e0 = self.joules()
         t0 = time.perf_counter()
+        if th is not None:
+            th.start()
         calls = 0
         while True:
             fn()
@@ -68,8 +97,21 @@ class EnergyMeter:
             dt = time.perf_counter() - t0
             if dt >= min_seconds:
                 break
+        if th is not None:
+            stop.set()
+            th.join()
         e1 = self.joules()
-        return calls, dt, (None if e0 is None or e1 is None else e1 - e0)
+        return calls, dt, (None if e0 is None or e1 is None else e1 - e0), mean_clock_mhz(samples)
+
+
+def mean_clock_mhz(samples):
+    """Mean shader clock (MHz) over clock samples, each a list of per-XCD
+    readings; readings that are not numbers in the chip's range (the metrics
+    table marks missing values with "N/A" or 0xFFFF) are left out.  None
+    when no reading is valid."""
+    vals = [float(v) for smp in samples for v in smp
+            if isinstance(v, (int, float)) and not isinstance(v, bool) and 0 < v < 10000]
+    return round(sum(vals) / len(vals), 1) if vals else None
 
 
 def report(calls: int, seconds: float, joules, tokens_per_call: int) -> dict:

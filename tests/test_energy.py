@@ -49,3 +49,11 @@ def test_report_without_reading(joules):
     assert out["calls"] == 4
     assert out["joules"] is None and out["avg_power_w"] is None
     assert out["joules_per_token"] is None and out["mwh_per_500b_tokens"] is None
+
+
+def test_mean_clock_skips_invalid_readings():
+    # per-XCD samples; "N/A", 0xFFFF and None mark readings the firmware did not fill
+    samples = [[2000, 2100, "N/A", 65535], [1900, None, 2000, 2000]]
+    assert energy.mean_clock_mhz(samples) == pytest.approx((2000 + 2100 + 1900 + 2000 + 2000) / 5, abs=0.05)
+    assert energy.mean_clock_mhz([]) is None
+    assert energy.mean_clock_mhz([["N/A"], [65535]]) is None
