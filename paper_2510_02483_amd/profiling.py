@@ -2,7 +2,7 @@
 
     python -m paper_2510_02483_amd.profiling stats DIR OUT.txt --cmd "..."
     python -m paper_2510_02483_amd.profiling traffic --kernel NAME --fetch DIR --write DIR \
-        --copy-fetch DIR --copy-write DIR --copy-bytes N --out OUT.txt --cmd "..."
+        --copy-fetch DIR --copy-write DIR --copy-bytes N --out OUT.txt --cmd "..." [--trace DIR --trace-cmd "..."]
 
     python -m paper_2510_02483_amd.profiling launches DIR OUT.txt --cmd "..."
     python -m paper_2510_02483_amd.profiling counters --kernel NAME --cus 256 --simds 4 --xcds 8 OUT.txt DIR... --cmd "..."
@@ -210,6 +210,24 @@ def counters(a):
     print("\n".join(lines))
 
 
+def _mean_duration_us(directory: str, kernel: str, launch: str | None = None):
+    """Mean duration (us) of a dispatch of `kernel` (substring of the name)
+    in a --kernel-trace run or, with `launch`, of that labelled launch of the
+    block step (its dispatches summed per step)."""
+    rows = _csv(directory, "kernel_trace.csv")
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    dur = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-3 for r in rows]
+    if launch is not None:
+        steps = label_steps([r["Kernel_Name"] for r in rows])
+        vals = [sum(dur[i] for i, lab in seq if lab == launch) for seq in steps]
+        vals = [v for v in vals if v > 0]
+    else:
+        vals = [d for r, d in zip(rows, dur) if kernel in r["Kernel_Name"]]
+    if not vals:
+        raise ValueError(f"no dispatches of {launch or kernel!r} in {directory}")
+    return sum(vals) / len(vals), len(vals)
+
+
 def traffic(a):
     fetch_kib, nf = _counter_per_dispatch(a.fetch, "FETCH_SIZE", a.kernel, a.launch)
     write_kib, nw = _counter_per_dispatch(a.write, "WRITE_SIZE", a.kernel, a.launch)
@@ -229,7 +247,14 @@ def traffic(a):
              f"copy calibration ({a.copy_bytes} bytes read and written): FETCH_SIZE {cf_kib:.1f} KiB, "
              f"WRITE_SIZE {cw_kib:.1f} KiB -> scale {f_scale:.4f} / {w_scale:.4f}",
              f"traffic per launch: fetch {fetch_b / 1e6:.1f} MB + write {write_b / 1e6:.1f} MB = "
-             f"{(fetch_b + write_b) / 1e6:.1f} MB", f"kernel sources hash: {entry['sources_hash']}"]
+             f"{(fetch_b + write_b) / 1e6:.1f} MB"]
+    if a.trace:
+        us, nd = _mean_duration_us(a.trace, a.kernel, a.launch)
+        entry["mean_us"] = us
+        entry["achieved_gbps"] = (fetch_b + write_b) / (us * 1e-6) / 1e9
+        lines.append(f"mean duration {us:.1f} us ({nd} dispatches of {a.trace_cmd or a.trace}): "
+                     f"achieved {entry['achieved_gbps']:.0f} GB/s of HBM-side traffic (L2 misses)")
+    lines.append(f"kernel sources hash: {entry['sources_hash']}")
     with open(a.out, "w") as f:
         f.write("\n".join(lines) + "\n")
     data = {}
@@ -261,6 +286,8 @@ def main():
     t.add_argument("--copy-bytes", type=float, required=True)
     t.add_argument("--out", required=True)
     t.add_argument("--cmd", required=True)
+    t.add_argument("--trace", default=None, help="a --kernel-trace run of the same workload, for durations and GB/s")
+    t.add_argument("--trace-cmd", default=None, help="the command of that run, for the summary")
     c = sub.add_parser("counters")
     c.add_argument("--kernel", required=True)
     c.add_argument("--cus", type=int, default=256)
