@@ -62,7 +62,6 @@ constexpr int KT = 64;                      // tile depth
 constexpr int KSTEPS = KT / 16;             // MFMA k-steps per tile
 constexpr int TILE_ELEMS = 256 * KT;        // LDS region of one k-strided operand tile (32 KB)
 constexpr int KC_PITCH = 1040;              // bytes per 1 KB block of a k-contiguous tile (16 B of padding)
-constexpr int GROUP_M = 8;                  // tile rows per group in the launch order
 constexpr int EPI_ROPE64 = 100;             // EPI_ROPE for 64-wide heads
 constexpr uint32_t OOB = LS_OOB;
 #ifndef GEMM_LOAD_SPAN_PCT
@@ -75,20 +74,27 @@ constexpr uint32_t OOB = LS_OOB;
 
 // Launch order: workgroups are handed to the 8 XCDs round-robin, so first
 // renumber them so that each XCD receives a contiguous range of logical tiles,
-// then walk the tiles in groups of GROUP_M tile rows so that the tiles an XCD
+// then walk the tiles in groups of group_m tile rows so that the tiles an XCD
 // works on at once share A rows and B columns in its L2.
-LS_DEV void map_tile(int wg, int tiles_m, int tiles_n, int& tm, int& tn) {
+LS_DEV void map_tile(int wg, int tiles_m, int tiles_n, int group_m, int& tm, int& tn) {
   const int nwg = tiles_m * tiles_n;
   const int q = nwg >> 3, r = nwg & 7, xcd = wg & 7, idx = wg >> 3;
   const int logical = (xcd < r ? xcd * (q + 1) : r * (q + 1) + (xcd - r) * q) + idx;
-  const int group = GROUP_M * tiles_n;
+  const int group = group_m * tiles_n;
   const int g = logical / group;
-  const int first_m = g * GROUP_M;
-  const int gm = min(tiles_m - first_m, GROUP_M);
+  const int first_m = g * group_m;
+  const int gm = min(tiles_m - first_m, group_m);
   const int in_g = logical - g * group;
   tm = first_m + in_g % gm;
   tn = in_g / gm;
 }
+
+// Tile rows per group of the launch order for BM x BN tiles.  The 32
+// workgroups an XCD runs at once (one per CU) then cover g tile rows x 32/g
+// tile columns and stream g A panels of BM rows and 32/g B panels of BN rows
+// through its L2 along K: g is the one of 4 and 8 with the fewer panel rows
+// g BM + (32/g) BN (8 on a tie), i.e. 4 for 256 x 192 tiles, 8 for 192 x 256.
+constexpr int group_rows(int bm, int bn) { return 4 * bm + 8 * bn < 8 * bm + 4 * bn ? 4 : 8; }
 
 // LDS swizzles (XOR on the 16-byte chunk index).  The LDS serves 16 lanes of a
 // 16-byte read (32 lanes of an 8-byte read) per clock across 64 banks, so:
@@ -307,7 +313,7 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_kernel(GemmArgs p) {
   const int ks = EPI == EPI_F32 ? p.ksplit : 1;
   const int slice = ks > 1 ? (int)blockIdx.x / (tiles_m * tiles_n) : 0;
   int tm, tn;
-  map_tile((int)blockIdx.x - slice * tiles_m * tiles_n, tiles_m, tiles_n, tm, tn);
+  map_tile((int)blockIdx.x - slice * tiles_m * tiles_n, tiles_m, tiles_n, p.group_m, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
   const int K = p.K;
 
@@ -753,7 +759,9 @@ constexpr int waves_of() {
   return BM == 256 && (!AK || (!BKC && (EPI == EPI_BF16 || EPI == EPI_GLU_BWD))) ? 8 : 4;
 }
 template <bool AK, bool BKC, int EPI, int BM, int BN, int NW = waves_of<AK, BKC, EPI, BM>()>
-hipError_t launch(const GemmArgs& a, hipStream_t s) {
+hipError_t launch(const GemmArgs& args, hipStream_t s) {
+  GemmArgs a = args;
+  a.group_m = group_rows(BM, BN);
   const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
   hipLaunchKernelGGL((gemm_kernel<AK, BKC, EPI, BM, BN, NW>), dim3(tiles * a.ksplit), dim3(NW * 64), 0, s, a);
   return hipGetLastError();

@@ -57,6 +57,7 @@ struct GemmArgs {
   float* kpart = nullptr;
   int64_t kpart_floats = 0;
   int ksplit = 1;  // slices of K (set by gemm())
+  int group_m = 8;  // tile rows per group of the launch order (set by the launch)
 };
 
 hipError_t gemm(const GemmArgs& a, hipStream_t s);
