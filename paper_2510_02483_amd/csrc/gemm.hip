@@ -49,6 +49,7 @@
 #include <algorithm>
 #include <atomic>
 #include <type_traits>
+#include <vector>
 
 #include "common.h"
 #include "kernels.h"
@@ -76,25 +77,21 @@ constexpr uint32_t OOB = LS_OOB;
 // renumber them so that each XCD receives a contiguous range of logical tiles,
 // then walk the tiles in groups of group_m tile rows so that the tiles an XCD
 // works on at once share A rows and B columns in its L2.
-LS_DEV void map_tile(int wg, int tiles_m, int tiles_n, int group_m, int& tm, int& tn) {
+// (Also run on the host, to pick group_m.)
+__host__ __device__ inline void map_tile(int wg, int tiles_m, int tiles_n, int group_m, int& tm, int& tn) {
   const int nwg = tiles_m * tiles_n;
   const int q = nwg >> 3, r = nwg & 7, xcd = wg & 7, idx = wg >> 3;
   const int logical = (xcd < r ? xcd * (q + 1) : r * (q + 1) + (xcd - r) * q) + idx;
   const int group = group_m * tiles_n;
   const int g = logical / group;
   const int first_m = g * group_m;
-  const int gm = min(tiles_m - first_m, group_m);
+  const int gm = tiles_m - first_m < group_m ? tiles_m - first_m : group_m;
   const int in_g = logical - g * group;
   tm = first_m + in_g % gm;
   tn = in_g / gm;
 }
 
-// Tile rows per group of the launch order for BM x BN tiles.  The 32
-// workgroups an XCD runs at once (one per CU) then cover g tile rows x 32/g
-// tile columns and stream g A panels of BM rows and 32/g B panels of BN rows
-// through its L2 along K: g is the one of 4 and 8 with the fewer panel rows
-// g BM + (32/g) BN (8 on a tie), i.e. 4 for 256 x 192 tiles, 8 for 192 x 256.
-constexpr int group_rows(int bm, int bn) { return 4 * bm + 8 * bn < 8 * bm + 4 * bn ? 4 : 8; }
+int group_rows(int M, int N, int K, int bm, int bn);
 
 // LDS swizzles (XOR on the 16-byte chunk index).  The LDS serves 16 lanes of a
 // 16-byte read (32 lanes of an 8-byte read) per clock across 64 banks, so:
@@ -761,7 +758,7 @@ constexpr int waves_of() {
 template <bool AK, bool BKC, int EPI, int BM, int BN, int NW = waves_of<AK, BKC, EPI, BM>()>
 hipError_t launch(const GemmArgs& args, hipStream_t s) {
   GemmArgs a = args;
-  a.group_m = group_rows(BM, BN);
+  a.group_m = group_rows(a.M, a.N, a.K, BM, BN);
   const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
   hipLaunchKernelGGL((gemm_kernel<AK, BKC, EPI, BM, BN, NW>), dim3(tiles * a.ksplit), dim3(NW * 64), 0, s, a);
   return hipGetLastError();
@@ -793,6 +790,47 @@ int compute_units() {
     return v;
   }();
   return n;
+}
+
+// Tile rows per group of the launch order (map_tile) for an M x N x K product
+// in BM x BN tiles.  Two caches decide it.  The workgroups an XCD runs at once
+// (one per CU, 32) cover g tile rows x 32/g tile columns and stream g A panels
+// of BM rows and 32/g B panels of BN rows along K through its 4 MB L2: fewer
+// panel rows, fewer L2 misses (4 for 256 x 192 tiles, 8 for 192 x 256).  And
+// the panels the whole chip reads in its first round of workgroups should fit
+// the 256 MB last-level cache, or every round fetches them from HBM again:
+// for K = 16384 and 368 MB of operands only g = 2 keeps a round within it.
+// So: among g = 8, 4, 2 whose first round fits, the fewest panel rows (the
+// larger g on a tie); if none fits, the smallest first-round footprint.
+int group_rows(int M, int N, int K, int bm, int bn) {
+  const int tiles_m = (M + bm - 1) / bm, tiles_n = (N + bn - 1) / bn;
+  const int ncu = compute_units(), round = std::min(tiles_m * tiles_n, ncu), per_xcd = std::max(ncu / 8, 1);
+  constexpr int64_t LLC_BYTES = (int64_t)256 << 20;
+  int best = 8;
+  bool best_fits = false;
+  int64_t best_rows = 0, best_bytes = 0;
+  std::vector<char> used_m(tiles_m), used_n(tiles_n);
+  for (int g : {8, 4, 2}) {
+    std::fill(used_m.begin(), used_m.end(), 0);
+    std::fill(used_n.begin(), used_n.end(), 0);
+    for (int wg = 0; wg < round; ++wg) {
+      int tm, tn;
+      map_tile(wg, tiles_m, tiles_n, g, tm, tn);
+      used_m[tm] = used_n[tn] = 1;
+    }
+    const int64_t panels = (int64_t)std::count(used_m.begin(), used_m.end(), 1) * bm +
+                           (int64_t)std::count(used_n.begin(), used_n.end(), 1) * bn;
+    const int64_t bytes = panels * K * 2, rows = (int64_t)g * bm + (int64_t)(per_xcd / g) * bn;
+    const bool fits = bytes <= LLC_BYTES;
+    const bool better = g == 8 || (fits && !best_fits) || (fits == best_fits && (fits ? rows < best_rows : bytes < best_bytes));
+    if (better) {
+      best = g;
+      best_fits = fits;
+      best_rows = rows;
+      best_bytes = bytes;
+    }
+  }
+  return best;
 }
 
 std::atomic<int> g_tile_override{0};  // 0: automatic, else 1000 * BM + BN
