@@ -592,25 +592,8 @@ int run_mlp_bwd(const ls_block_cfg& cfg, const Dims& m, const bf16_t* x2, const 
     g.glu_I = (int)m.I;
     LS_STEP("dact", st, ls::gemm(g, st));
   }
-  {  // dWd (+)= dy^T act
-    ls::GemmArgs g;
-    g.M = (int)m.H;
-    g.N = (int)m.I;
-    g.K = (int)m.T;
-    g.A = dy;
-    g.lda = m.H;
-    g.a_kcontig = false;
-    g.B[0] = act;
-    g.ldb = m.I;
-    g.b_kcontig = false;
-    g.epi = ls::EPI_F32;
-    g.F[0] = gr->wd;
-    g.ldf = m.I;
-    g.accumulate = accumulate;
-    g.kpart = at<float>(ws, wl.kpart);
-    g.kpart_floats = wl.kpart_floats;
-    LS_STEP("dWd", st, ls::gemm(g, st));
-  }
+  // dh2 and dWg/dWu follow dact, which has just written dgu, so they read
+  // much of it from the last-level cache; dWd (dy and act only) goes last.
   {  // dh2 = dg Wg + du Wu
     ls::GemmArgs g;
     g.M = (int)m.T;
@@ -648,6 +631,25 @@ int run_mlp_bwd(const ls_block_cfg& cfg, const Dims& m, const bf16_t* x2, const 
     g.kpart = at<float>(ws, wl.kpart);
     g.kpart_floats = wl.kpart_floats;
     LS_STEP("dWg/dWu", st, ls::gemm(g, st));
+  }
+  {  // dWd (+)= dy^T act
+    ls::GemmArgs g;
+    g.M = (int)m.H;
+    g.N = (int)m.I;
+    g.K = (int)m.T;
+    g.A = dy;
+    g.lda = m.H;
+    g.a_kcontig = false;
+    g.B[0] = act;
+    g.ldb = m.I;
+    g.b_kcontig = false;
+    g.epi = ls::EPI_F32;
+    g.F[0] = gr->wd;
+    g.ldf = m.I;
+    g.accumulate = accumulate;
+    g.kpart = at<float>(ws, wl.kpart);
+    g.kpart_floats = wl.kpart_floats;
+    LS_STEP("dWd", st, ls::gemm(g, st));
   }
   LS_STEP("rmsnorm bwd", st,
           ls::rmsnorm_bwd(m.T, (int)m.H, x2, (const bf16_t*)w->mlp_norm, r2, dh2, dy, dx2, gr->mlp_norm, accumulate,

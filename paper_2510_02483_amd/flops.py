@@ -62,7 +62,7 @@ def stack_fwd_bwd_flops(sc: StackConfig, causal: bool = True) -> float:
 # Labelled launches of one block step (forward, then the MLP and attention
 # backward passes) in the order the library issues them.
 BLOCK_LAUNCHES = ("rmsnorm fwd", "qkv projection", "attention fwd", "output projection", "gate/up projection",
-                  "down projection", "dact", "dWd", "dh2", "dWg/dWu", "rmsnorm bwd", "dO", "dWo", "attention bwd",
+                  "down projection", "dact", "dh2", "dWg/dWu", "dWd", "rmsnorm bwd", "dO", "dWo", "attention bwd",
                   "dh1", "dWqkv")
 
 

@@ -71,8 +71,8 @@ def stats(directory: str, out: str, cmd: str, top: int = 25):
 
 # The matrix products of one block step in issue order (each may be followed
 # by the reduction of its split K, which counts as part of it).
-GEMM_ORDER = ("qkv projection", "output projection", "gate/up projection", "down projection", "dact", "dWd", "dh2",
-              "dWg/dWu", "dO", "dWo", "dh1", "dWqkv")
+GEMM_ORDER = ("qkv projection", "output projection", "gate/up projection", "down projection", "dact", "dh2", "dWg/dWu",
+              "dWd", "dO", "dWo", "dh1", "dWqkv")
 
 
 def label_steps(names):

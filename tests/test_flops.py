@@ -71,7 +71,7 @@ def test_profile_launch_labelling():
     from paper_2510_02483_amd import profiling
     g = "gemm_kernel<...>"
     step = (["rmsnorm_fwd_kernel<6>", "rope_table_kernel", g, "attn_fwd_kernel<128>", g, "rmsnorm_fwd_kernel<6>", g, g,
-             g, g, "kpart_reduce_kernel", g, g, "rmsnorm_bwd_kernel<6>", "column_sum_kernel", "rope_table_kernel", g, g,
+             g, g, g, g, "kpart_reduce_kernel", "rmsnorm_bwd_kernel<6>", "column_sum_kernel", "rope_table_kernel", g, g,
              "attn_bwd_pre_kernel<128>", "attn_bwd_dkdv_kernel<128, true>", "attn_bwd_dkdv_reduce<128>",
              "attn_bwd_dq_kernel<128>", g, g, "rmsnorm_bwd_kernel<6>", "column_sum_kernel"])
     names = ["FillFunctor"] + step + step + ["copyBuffer"]
@@ -79,7 +79,8 @@ def test_profile_launch_labelling():
     assert len(steps) == 2
     labels = [lab for _, lab in steps[0]]
     assert labels[2] == "qkv projection" and labels[3] == "attention fwd"
-    assert labels[9:11] == ["dWd", "dWd"]  # the split-K reduction belongs to its product
+    assert labels[8:11] == ["dact", "dh2", "dWg/dWu"]
+    assert labels[11:13] == ["dWd", "dWd"]  # the split-K reduction belongs to its product
     assert labels.count("attention bwd") == 4 and labels.count("rmsnorm bwd") == 4
     assert [lab for lab in labels if lab in profiling.GEMM_ORDER][-1] == "dWqkv"
     assert steps[1][0][0] == 1 + len(step)
