@@ -21,19 +21,17 @@ namespace {
 
 constexpr int kVersion = 100;  // 0.1.0
 
-thread_local std::string g_last_error;
+thread_local char g_last_error[512];  // a fixed buffer: reporting an error allocates nothing
 
 // Largest matrix in bytes (exclusive): the kernels' buffer resources are
 // clamped to 2047 MiB.
 constexpr int64_t kMaxBytes = (int64_t)0x7ff00000;
 
 int fail(int code, const char* fmt, ...) {
-  char buf[512];
   va_list ap;
   va_start(ap, fmt);
-  vsnprintf(buf, sizeof(buf), fmt, ap);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
   va_end(ap);
-  g_last_error = buf;
   return code;
 }
 
@@ -149,22 +147,25 @@ bool overlaps(const Range& a, const Range& b) {
 }
 
 // every output range against every input range and every other output range
-int check_ranges(const std::vector<Range>& in, const std::vector<Range>& out) {
-  for (const Range& r : in) {
-    if (!r.p) return fail(LS_ERR_NULL, "%s is NULL", r.name);
-    if (misaligned(r.p)) return fail(LS_ERR_ALIGN, "%s is not 16-byte aligned", r.name);
+int check_ranges(const Range* in, size_t nin, const Range* out, size_t nout) {
+  for (size_t i = 0; i < nin; ++i) {
+    if (!in[i].p) return fail(LS_ERR_NULL, "%s is NULL", in[i].name);
+    if (misaligned(in[i].p)) return fail(LS_ERR_ALIGN, "%s is not 16-byte aligned", in[i].name);
   }
-  for (const Range& r : out) {
-    if (!r.p) return fail(LS_ERR_NULL, "%s is NULL", r.name);
-    if (misaligned(r.p)) return fail(LS_ERR_ALIGN, "%s is not 16-byte aligned", r.name);
+  for (size_t i = 0; i < nout; ++i) {
+    if (!out[i].p) return fail(LS_ERR_NULL, "%s is NULL", out[i].name);
+    if (misaligned(out[i].p)) return fail(LS_ERR_ALIGN, "%s is not 16-byte aligned", out[i].name);
   }
-  for (size_t i = 0; i < out.size(); ++i) {
-    for (const Range& r : in)
-      if (overlaps(out[i], r)) return fail(LS_ERR_ALIAS, "%s overlaps %s", out[i].name, r.name);
-    for (size_t j = i + 1; j < out.size(); ++j)
+  for (size_t i = 0; i < nout; ++i) {
+    for (size_t j = 0; j < nin; ++j)
+      if (overlaps(out[i], in[j])) return fail(LS_ERR_ALIAS, "%s overlaps %s", out[i].name, in[j].name);
+    for (size_t j = i + 1; j < nout; ++j)
       if (overlaps(out[i], out[j])) return fail(LS_ERR_ALIAS, "%s overlaps %s", out[i].name, out[j].name);
   }
   return LS_OK;
+}
+int check_ranges(const std::vector<Range>& in, const std::vector<Range>& out) {
+  return check_ranges(in.data(), in.size(), out.data(), out.size());
 }
 
 // ---- buffer layouts ------------------------------------------------------------
@@ -724,7 +725,7 @@ extern "C" {
 
 int ls_version(void) { return kVersion; }
 
-const char* ls_last_error(void) { return g_last_error.c_str(); }
+const char* ls_last_error(void) { return g_last_error; }
 
 const char* ls_status_string(int status) {
   switch (status) {
@@ -971,12 +972,13 @@ int ls_attn_core_bwd_noalloc(const ls_block_cfg* cfg, const ls_bf16* qkv, const 
   if (int e = check_core_cfg(cfg)) return e;
   const Dims m = dims_of(*cfg);
   const size_t need = ls::attn_bwd_workspace(attn_shape(m));
-  std::vector<Range> in{{qkv, (size_t)(m.T * m.Dqkv * 2), "qkv"},
-                        {o, (size_t)(m.T * m.Dq * 2), "o"},
-                        {lse, (size_t)(m.B * m.nq * m.S * 4), "lse"},
-                        {dout, (size_t)(m.T * m.Dq * 2), "dout"}};
-  std::vector<Range> out{{dqkv, (size_t)(m.T * m.Dqkv * 2), "dqkv"}};
-  if (int e = check_ranges(in, out)) return e;
+  // fixed arrays: this entry point allocates nothing, on the host either
+  const Range in[] = {{qkv, (size_t)(m.T * m.Dqkv * 2), "qkv"},
+                      {o, (size_t)(m.T * m.Dq * 2), "o"},
+                      {lse, (size_t)(m.B * m.nq * m.S * 4), "lse"},
+                      {dout, (size_t)(m.T * m.Dq * 2), "dout"}};
+  const Range out[] = {{dqkv, (size_t)(m.T * m.Dqkv * 2), "dqkv"}};
+  if (int e = check_ranges(in, 4, out, 1)) return e;
   if (need > (size_t)LS_ATTN_CORE_BWD_NOALLOC_SCRATCH)
     return fail(LS_ERR_WORKSPACE,
                 "this shape needs %zu bytes of scratch, beyond the library's %zu-byte array (use ls_attn_core_bwd "

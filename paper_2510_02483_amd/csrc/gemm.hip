@@ -49,7 +49,6 @@
 #include <algorithm>
 #include <atomic>
 #include <type_traits>
-#include <vector>
 
 #include "common.h"
 #include "kernels.h"
@@ -806,20 +805,22 @@ int group_rows(int M, int N, int K, int bm, int bn) {
   const int tiles_m = (M + bm - 1) / bm, tiles_n = (N + bn - 1) / bn;
   const int ncu = compute_units(), round = std::min(tiles_m * tiles_n, ncu), per_xcd = std::max(ncu / 8, 1);
   constexpr int64_t LLC_BYTES = (int64_t)256 << 20;
+  constexpr int MAX_TILES = 4096;  // per dimension (no allocation in a call): larger grids keep 8
+  if (tiles_m > MAX_TILES || tiles_n > MAX_TILES) return 8;
   int best = 8;
   bool best_fits = false;
   int64_t best_rows = 0, best_bytes = 0;
-  std::vector<char> used_m(tiles_m), used_n(tiles_n);
+  char used_m[MAX_TILES], used_n[MAX_TILES];
   for (int g : {8, 4, 2}) {
-    std::fill(used_m.begin(), used_m.end(), 0);
-    std::fill(used_n.begin(), used_n.end(), 0);
+    std::fill(used_m, used_m + tiles_m, 0);
+    std::fill(used_n, used_n + tiles_n, 0);
     for (int wg = 0; wg < round; ++wg) {
       int tm, tn;
       map_tile(wg, tiles_m, tiles_n, g, tm, tn);
       used_m[tm] = used_n[tn] = 1;
     }
-    const int64_t panels = (int64_t)std::count(used_m.begin(), used_m.end(), 1) * bm +
-                           (int64_t)std::count(used_n.begin(), used_n.end(), 1) * bn;
+    const int64_t panels = (int64_t)std::count(used_m, used_m + tiles_m, 1) * bm +
+                           (int64_t)std::count(used_n, used_n + tiles_n, 1) * bn;
     const int64_t bytes = panels * K * 2, rows = (int64_t)g * bm + (int64_t)(per_xcd / g) * bn;
     const bool fits = bytes <= LLC_BYTES;
     const bool better = g == 8 || (fits && !best_fits) || (fits == best_fits && (fits ? rows < best_rows : bytes < best_bytes));
