@@ -194,9 +194,11 @@ LS_DEV void ks_setup(OpLoads<NL>& o, int col0, int cols, int64_t ld, int wave, i
 }
 
 // Offset of load l of a tile with `kvalid` valid k values (64 for a whole tile);
-// W: the width of a k-strided tile (unused for k-contiguous ones).
-template <bool KC, int NL, int W>
+// W: the width of a k-strided tile (unused for k-contiguous ones).  FULL: the
+// caller knows the tile is whole, so no lane is masked.
+template <bool KC, int NL, int W, bool FULL>
 LS_DEV uint32_t load_off(const OpLoads<NL>& o, int l, int kvalid, int wave) {
+  if constexpr (FULL) return o.voff[l];
   bool ok;
   if constexpr (KC) ok = (int)o.kpos[l & 1] < kvalid;
   else ok = (int)o.kpos[0] < kvalid - ks_row0<W>(wave * NL + l);
@@ -205,9 +207,9 @@ LS_DEV uint32_t load_off(const OpLoads<NL>& o, int l, int kvalid, int wave) {
 
 // Load l of an operand tile into the LDS block at byte address m0 + l KB
 // (m0: the wave's first block of the stage).
-template <bool KC, int NL, int W>
+template <bool KC, int NL, int W, bool FULL>
 LS_DEV void load_one(const OpLoads<NL>& o, int l, uint32_t soff, int kvalid, uint32_t m0, int wave) {
-  dma1(o.r, load_off<KC, NL, W>(o, l, kvalid, wave), soff, m0 + (KC ? (uint32_t)KC_PITCH : 1024u) * l);
+  dma1(o.r, load_off<KC, NL, W, FULL>(o, l, kvalid, wave), soff, m0 + (KC ? (uint32_t)KC_PITCH : 1024u) * l);
 }
 
 // Fragment of a k-contiguous tile (at byte address t): lane gets row `r`
@@ -286,7 +288,8 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_kernel(GemmArgs p) {
   // Fragments are read RA k-steps ahead of the MFMAs that use them (RA + 1
   // register buffers; with RA = 2 four, one per k-step of a tile), so that a
   // read delayed by the buffer->LDS writes does not hold up the matrix core.
-  constexpr int RA = GEMM_READ_AHEAD;
+  // Measured: two steps with one wave per SIMD, one with two waves per SIMD.
+  constexpr int RA = NW == 8 ? 1 : GEMM_READ_AHEAD;
   static_assert(RA == 1 || RA == 2, "read-ahead of one or two k-steps");
   constexpr int NBUF = RA == 1 ? 2 : 4;
   constexpr int BS = KSTEPS - RA;  // the k-step of a tile that holds the barrier
@@ -383,10 +386,12 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_kernel(GemmArgs p) {
   auto advance = [&]() { set_cursor(ck + kval); };
   const uint32_t lds0 = lds_offset(&lds[0]);
   const uint32_t ma = lds0 + wave * NA * (AK ? KC_PITCH : 1024), mb = lds0 + A_BYTES + wave * NB * (BKC ? KC_PITCH : 1024);
-  // Load q of the tile at the cursor (A loads first) into the stage at byte offset stage_off.
-  auto issue = [&](int q, uint32_t stage_off) {
-    if (q < NA) load_one<AK, NA, BM>(la, q, soa, kval, ma + stage_off, wave);
-    else load_one<BKC, NB, BN>(lb, q - NA, sob, kval, mb + stage_off, wave);
+  // Load q of the tile at the cursor (A loads first) into the stage at byte
+  // offset stage_off; full_c: std::true_type where that tile is known to be whole.
+  auto issue = [&](auto full_c, int q, uint32_t stage_off) {
+    constexpr bool FULL = decltype(full_c)::value;
+    if (q < NA) load_one<AK, NA, BM, FULL>(la, q, soa, kval, ma + stage_off, wave);
+    else load_one<BKC, NB, BN, FULL>(lb, q - NA, sob, kval, mb + stage_off, wave);
   };
 
   f32x16 acc[TM][TN];
@@ -424,8 +429,12 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_kernel(GemmArgs p) {
   // done reading this stage (its last fragments were read one step earlier),
   // so the loads of the tile after next can go into it while the MFMAs run.
   // Every instruction is pinned in place with scheduling barriers.
-  auto tile = [&](auto nx_c, int cur) {
+  // cur_c: the stage, a compile-time constant in the unrolled loop over whole
+  // tiles (every LDS address is then a register plus an immediate) or an int;
+  // full_c: every tile this one loads is whole (no lane masking).
+  auto tile = [&](auto nx_c, auto cur_c, auto full_c) {
     constexpr int NX = decltype(nx_c)::value;
+    const int cur = cur_c;
     const uint32_t here = (uint32_t)cur * STAGE_BYTES, there = (uint32_t)(cur ^ 1) * STAGE_BYTES;
     static_for<KSTEPS>([&](auto s_c) {
       constexpr int s = s_c;
@@ -447,12 +456,12 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_kernel(GemmArgs p) {
           constexpr int at = slot_of(q) + BS * NMF;  // tile-relative slot of load q (may be in the next tile)
           // the later loads of the next tile (its first ones went out in the previous tile)
           if constexpr (NX >= 1 && at >= KSTEPS * NMF && at - KSTEPS * NMF == s * NMF + i) {
-            issue(q, there);
+            issue(full_c, q, there);
             if constexpr (q == NL - 1) advance();
           }
           // the first loads of the tile after next, into this stage
           if constexpr (NX >= 2 && at < KSTEPS * NMF && at == s * NMF + i) {
-            issue(q, here);
+            issue(full_c, q, here);
             if constexpr (q == NL - 1) advance();
           }
         });
@@ -470,11 +479,11 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_kernel(GemmArgs p) {
   }();
   set_cursor(kbeg);
 #pragma unroll
-  for (int q = 0; q < NL; ++q) issue(q, 0);
+  for (int q = 0; q < NL; ++q) issue(std::false_type{}, q, 0);
   advance();
   if (nk > 1) {
 #pragma unroll
-    for (int q = 0; q < FIRST; ++q) issue(q, STAGE_BYTES);
+    for (int q = 0; q < FIRST; ++q) issue(std::false_type{}, q, STAGE_BYTES);
     if (FIRST == NL) advance();
     LS_WAIT_VMCNT(FIRST);
   } else {
@@ -486,10 +495,29 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_kernel(GemmArgs p) {
   for (int t = 0; t < RA; ++t)
 #pragma unroll
     for (int u = 0; u < NRU; ++u) read_unit(0, t, bufi(t), u);
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
   int kt = 0;
-  for (; kt + 2 < nk; ++kt) tile(std::integral_constant<int, 2>{}, kt & 1);
-  if (kt + 1 < nk) tile(std::integral_constant<int, 1>{}, kt++ & 1);
-  tile(std::integral_constant<int, 0>{}, kt & 1);
+  // Every tile of every k segment whole (k lengths multiples of the tile
+  // depth): no load masks, and with one wave per SIMD two tiles per pass, one
+  // per stage, so every fragment address is a register plus an immediate (with
+  // two waves per SIMD that copy of the loop needs more registers than a wave
+  // has and spills).
+  const bool whole = S1 % KT == 0 && (S2 - S1) % KT == 0 && (K - S2) % KT == 0;
+  if (whole) {
+    if constexpr (NW == 4) {
+      for (; kt + 3 < nk; kt += 2) {
+        tile(I2{}, I0{}, std::true_type{});
+        tile(I2{}, I1{}, std::true_type{});
+      }
+    } else {
+      for (; kt + 2 < nk; ++kt) tile(I2{}, kt & 1, std::true_type{});
+    }
+  }
+  for (; kt + 2 < nk; ++kt) tile(I2{}, kt & 1, std::false_type{});
+  if (kt + 1 < nk) tile(I1{}, kt++ & 1, std::false_type{});
+  tile(I0{}, kt & 1, std::false_type{});
   auto sync_tile = []() { sync_lds(); };
   sync_tile();  // every wave is done with both stages before they become staging space
 
