@@ -67,6 +67,9 @@ constexpr uint32_t OOB = LS_OOB;
 #ifndef GEMM_LOAD_SPAN_PCT
 #define GEMM_LOAD_SPAN_PCT 60  // share of a tile's MFMA slots over which its loads are spread
 #endif
+#ifndef GEMM_LOAD_SPAN_NT
+#define GEMM_LOAD_SPAN_NT 45  // the same for the forward (NT) products, whose loop has no transposing reads
+#endif
 #ifndef GEMM_READ_AHEAD
 #define GEMM_READ_AHEAD 2  // k-steps between a fragment read and its MFMAs
 #endif
@@ -283,7 +286,7 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_kernel(GemmArgs p) {
   // period is left for the last loads to arrive.
   constexpr int BAR_AT = NMF >= 16 ? 2 : 1;
   static_assert(BAR_AT + NRU <= NMF, "the next tile's first fragments are read within one k-step");
-  constexpr int LSPAN = (KSTEPS * NMF * GEMM_LOAD_SPAN_PCT) / 100;
+  constexpr int LSPAN = (KSTEPS * NMF * (AK && BKC ? GEMM_LOAD_SPAN_NT : GEMM_LOAD_SPAN_PCT)) / 100;
   static_assert(BAR_AT + LSPAN < KSTEPS * NMF, "every load is issued before the next barrier");
   // Fragments are read RA k-steps ahead of the MFMAs that use them (RA + 1
   // register buffers; with RA = 2 four, one per k-step of a tile), so that a
