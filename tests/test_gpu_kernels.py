@@ -14,10 +14,13 @@ from gpu_util import GRAD_TOL, OUT_TOL, bf16_randn, f64, fro_rel, max_rel, need_
 
 pytestmark = pytest.mark.gpu
 
-# the last shape has more output tiles than compute units (17 x 17 and more), so
-# its products run persistent: workgroups walk several tiles, ragged ones included
+# the 4104 x 4200 shape has more output tiles than compute units (17 x 17 and
+# more), so its products run persistent: workgroups walk several tiles, ragged
+# ones included.  K takes ragged tile counts (the masked loop) and whole ones of
+# 1, 2, 3, 9 and 10 tiles of 64 (the unmasked loop, which with one wave per SIMD
+# runs two tiles per pass: an odd count leaves one tile for the masked loop).
 GEMM_SHAPES = [(136, 264, 72), (520, 776, 1000), (256, 512, 640), (8, 8, 8), (1032, 264, 1376), (392, 584, 200),
-               (4104, 4200, 264)]
+               (4104, 4200, 264), (136, 200, 64), (264, 136, 128), (200, 264, 192), (264, 392, 576)]
 # workgroup tile shapes: automatic choice, then each forced shape (products
 # whose kernel has no such variant fall back to 256 x 256)
 GEMM_TILES = [(0, 0), (256, 256), (256, 192), (192, 256), (192, 192)]
