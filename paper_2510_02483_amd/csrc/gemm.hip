@@ -590,16 +590,25 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_kernel(GemmArgs p) {
       float* base = sg == 2 ? p.F[2] : (sg == 1 ? p.F[1] : p.F[0]);
       const int fs = sg == 2 ? p.f_start[2] : (sg == 1 ? p.f_start[1] : 0);
       float* row = kp ? kp + (int64_t)m * p.N : base + (int64_t)(m - fs) * p.ldf;
+      // the accumulated values of the row block, all loads in flight at once
+      // (one at a time, each load and store waited for the one before)
+      f32x4 old[TN][4];
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int n = nw + 32 * j + 8 * q + 4 * lh;
+          old[j][q] = f32x4{0.f, 0.f, 0.f, 0.f};
+          if (p.accumulate && !kp && m < p.M && n < p.N) old[j][q] = *(const f32x4*)(row + n);
+        }
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const int n = nw + 32 * j + 8 * q + 4 * lh;
-          f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
-          if (m < p.M && n < p.N) {
-            if (p.accumulate && !kp) v += *(const f32x4*)(row + n);
-            *(f32x4*)(row + n) = v;
-          }
+          const f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+          if (m < p.M && n < p.N) *(f32x4*)(row + n) = v + old[j][q];
         }
         __builtin_amdgcn_sched_barrier(0);
       }
@@ -607,10 +616,20 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_kernel(GemmArgs p) {
   } else if constexpr (EPI == EPI_RESID) {
     // Straight from the registers: the fp32 results are moved into 16-byte
     // row pieces (8 columns per lane), added to the residual (one 16-byte
-    // load) and rounded once.
+    // load each, a row block's loads issued together) and rounded once.
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
       const int m = mw + 32 * i + lr;
+      // the residual pieces of the row block, all loads in flight at once
+      u32x4 res[TN][2];
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int pp = 0; pp < 2; ++pp) {
+          const int n = nw + 32 * j + 16 * pp + 8 * lh;
+          res[j][pp] = m < p.M && n < p.N ? *(const u32x4*)(p.R + (int64_t)m * p.ldc + n) : u32x4{0u, 0u, 0u, 0u};
+        }
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int j = 0; j < TN; ++j)
 #pragma unroll
@@ -621,7 +640,7 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_kernel(GemmArgs p) {
                    f32x4{acc[i][j][8 * pp + 4], acc[i][j][8 * pp + 5], acc[i][j][8 * pp + 6], acc[i][j][8 * pp + 7]},
                    lo, hi);
           if (m < p.M && n < p.N) {
-            const u32x4 rw = *(const u32x4*)(p.R + (int64_t)m * p.ldc + n);
+            const u32x4 rw = res[j][pp];
             *(u32x4*)(p.C + (int64_t)m * p.ldc + n) =
                 u32x4{pack_bf2(lo[0] + bf_lo(rw[0]), lo[1] + bf_hi(rw[0])), pack_bf2(lo[2] + bf_lo(rw[1]), lo[3] + bf_hi(rw[1])),
                       pack_bf2(hi[0] + bf_lo(rw[2]), hi[1] + bf_hi(rw[2])), pack_bf2(hi[2] + bf_lo(rw[3]), hi[3] + bf_hi(rw[3]))};
