@@ -774,6 +774,22 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_kernel(GemmArgs p) {
         const int pos = (m < p.M ? m : 0) % p.seq;
         const float* cs = p.rope_cs + (int64_t)pos * HALF;
         const float* sn = p.rope_cs + (int64_t)p.seq * HALF + (int64_t)pos * HALF;
+        // cos and sin of the lane's 4 consecutive angle indices at each 32-column
+        // offset of the first half of a head (16-byte loads), all in flight at
+        // once before the rotations that use them
+        f32x4 cpre[JP][4], spre[JP][4];
+#pragma unroll
+        for (int d = 0; d < JP; ++d)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            cpre[d][q] = f32x4{1.f, 1.f, 1.f, 1.f};
+            spre[d][q] = f32x4{0.f, 0.f, 0.f, 0.f};
+            if (nw < p.rope_cols) {
+              cpre[d][q] = *(const f32x4*)(cs + 32 * d + 8 * q + 4 * lh);
+              spre[d][q] = *(const f32x4*)(sn + 32 * d + 8 * q + 4 * lh);
+            }
+          }
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
           const bool rot = nw + 32 * j < p.rope_cols;
@@ -782,12 +798,7 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_kernel(GemmArgs p) {
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
             float lo[4], hi[4];
-            // cos and sin of the lane's 4 consecutive angle indices (16-byte loads)
-            f32x4 c4 = {1.f, 1.f, 1.f, 1.f}, s4 = {0.f, 0.f, 0.f, 0.f};
-            if (rot && j + JP < TN) {
-              c4 = *(const f32x4*)(cs + dcol + 8 * q + 4 * lh);
-              s4 = *(const f32x4*)(sn + dcol + 8 * q + 4 * lh);
-            }
+            const f32x4 c4 = cpre[(dcol / 32) % JP][q], s4 = spre[(dcol / 32) % JP][q];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
               const float x1 = acc[i][j][4 * q + e];
