@@ -653,46 +653,47 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_kernel(GemmArgs p) {
     // subtiles j = 0, 1 hold gate columns, j = 2, 3 the up columns of the same 64 features
     const int col0 = nw / 2;  // first feature of the wave tile
     const int nvalid = p.glu_I - col0;
-    if (p.C) {  // the gate and up outputs themselves (kept for the backward pass)
+    // One 32-row block at a time: its gate and up values (rows 0..31 of the
+    // staging region, [g(64) | u(64)]) and its act values (rows 32..63, 64
+    // columns) are staged, then stored while the next block is computed; each
+    // block's accumulators are done with after it (fewer live registers than
+    // staging all gate/up rows first and computing act from them afterwards).
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            float v[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * q + e];
-            put4(32 * i + lr, 32 * j + 8 * q + 4 * lh, v);  // [g(64) | u(64)] per row
-          }
-#pragma unroll 4
-      for (int t = 0; t < WM / 4; ++t) {
-        const int c = lane + 64 * t, r = c >> 4, cc = c & 15;
-        const u32x4 v = *(const u32x4*)&stg[sb(r, cc * 8)];
-        const int f = (cc & 7) * 8;  // feature offset within the 64
-        if (mw + r < p.M && f < nvalid)
-          *(u32x4*)(p.C + (int64_t)(mw + r) * p.ldc + (cc < 8 ? 0 : p.glu_I) + col0 + f) = v;
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
+    for (int i = 0; i < TM; ++i) {
 #pragma unroll
       for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          float v[4];
+          float g[4], u[4], a[4];
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const float g = acc[i][j][4 * q + e], u = acc[i][j + 2][4 * q + e];
-            v[e] = silu_f(g) * u;
+            g[e] = acc[i][j][4 * q + e];
+            u[e] = acc[i][j + 2][4 * q + e];
+            a[e] = silu_f(g[e]) * u[e];
           }
-          put4(32 * i + lr, 32 * j + 8 * q + 4 * lh, v);
+          if (p.C) {
+            put4(lr, 32 * j + 8 * q + 4 * lh, g);
+            put4(lr, 64 + 32 * j + 8 * q + 4 * lh, u);
+          }
+          put4(32 + lr, 32 * j + 8 * q + 4 * lh, a);
         }
-#pragma unroll 4
-    for (int t = 0; t < WM / 8; ++t) {
-      const int c = lane + 64 * t, r = c >> 3, cc = c & 7;
-      const u32x4 v = *(const u32x4*)&stg[sb(r, cc * 8)];
-      if (mw + r < p.M && cc * 8 < nvalid) *(u32x4*)(p.act + (int64_t)(mw + r) * p.glu_I + col0 + cc * 8) = v;
+      const int mb = mw + 32 * i;
+      if (p.C) {
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+          const int c = lane + 64 * t, r = c >> 4, cc = c & 15;
+          const u32x4 v = *(const u32x4*)&stg[sb(r, cc * 8)];
+          const int f = (cc & 7) * 8;  // feature offset within the 64
+          if (mb + r < p.M && f < nvalid)
+            *(u32x4*)(p.C + (int64_t)(mb + r) * p.ldc + (cc < 8 ? 0 : p.glu_I) + col0 + f) = v;
+        }
+      }
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int c = lane + 64 * t, r = c >> 3, cc = c & 7;
+        const u32x4 v = *(const u32x4*)&stg[sb(32 + r, cc * 8)];
+        if (mb + r < p.M && cc * 8 < nvalid) *(u32x4*)(p.act + (int64_t)(mb + r) * p.glu_I + col0 + cc * 8) = v;
+      }
     }
   } else if constexpr (EPI == EPI_GLU_BWD) {
     static_assert(WN == 128, "the gate/up staging covers 128-column wave tiles");
