@@ -208,7 +208,7 @@ MlpSaved mlp_saved_layout(const Dims& m) {
   return s;
 }
 
-size_t norm_partial_bytes(const Dims& m) { return (size_t)ls::rmsnorm_bwd_parts(m.T) * m.H * 4; }
+size_t norm_partial_bytes(const Dims& m) { return (size_t)ls::rmsnorm_bwd_parts(m.T, (int)m.H) * m.H * 4; }
 
 ls::AttnShape attn_shape(const Dims& m) {
   return ls::AttnShape{(int)m.B, (int)m.S, (int)m.nq, (int)m.nkv, (int)m.dp, (int)m.d};
@@ -1015,7 +1015,7 @@ int ls_rmsnorm_fwd(int64_t rows, int32_t hidden, float eps, const ls_bf16* x, co
 
 size_t ls_rmsnorm_bwd_workspace(int64_t rows, int32_t hidden) {
   if (rows <= 0 || hidden <= 0) return 0;
-  return (size_t)ls::rmsnorm_bwd_parts(rows) * hidden * 4;
+  return (size_t)ls::rmsnorm_bwd_parts(rows, (int)hidden) * hidden * 4;
 }
 
 int ls_rmsnorm_bwd(int64_t rows, int32_t hidden, const ls_bf16* x, const ls_bf16* gamma, const float* r,

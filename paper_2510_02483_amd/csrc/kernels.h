@@ -71,8 +71,8 @@ int gemm_tile_override(int bm, int bn);
 // ---- RMSNorm ------------------------------------------------------------------
 hipError_t rmsnorm_fwd(int64_t rows, int hidden, float eps, const bf16_t* x, const bf16_t* gamma,
                        bf16_t* h, float* r, hipStream_t s);
-// Partial buffer of rmsnorm_bwd: rmsnorm_bwd_parts(rows) x hidden floats.
-int rmsnorm_bwd_parts(int64_t rows);
+// Partial buffer of rmsnorm_bwd: rmsnorm_bwd_parts(rows, hidden) x hidden floats.
+int rmsnorm_bwd_parts(int64_t rows, int hidden);
 hipError_t rmsnorm_bwd(int64_t rows, int hidden, const bf16_t* x, const bf16_t* gamma, const float* r,
                        const bf16_t* dh, const bf16_t* dres, bf16_t* dx, float* dgamma, int accumulate,
                        float* partial, hipStream_t s);

@@ -81,12 +81,18 @@ __global__ __launch_bounds__(64 * BWD_WAVES) void rmsnorm_bwd_kernel(int64_t row
   __shared__ float red[CH * 512];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int chunks = hidden / 8;
-  u32x4 gv[CH];
+  // Rows wider than 3072 (more than 6 chunks per lane): gamma and the
+  // residual gradient are read where they are used instead of being held for
+  // the whole row, so that x, dh and the gain-gradient sums fit the registers
+  // (holding all five spills from 7 chunks on; past 8 chunks the wide kernel
+  // below takes over).
+  constexpr bool WIDE = CH > 6;
+  auto gamma_chunk = [&](int c) { return c < chunks ? *(const u32x4*)(gamma + c * 8) : u32x4{0u, 0u, 0u, 0u}; };
+  u32x4 gv[WIDE ? 1 : CH];
   float gsum[CH][8];
 #pragma unroll
   for (int i = 0; i < CH; ++i) {
-    const int c = lane + 64 * i;
-    gv[i] = c < chunks ? *(const u32x4*)(gamma + c * 8) : u32x4{0u, 0u, 0u, 0u};
+    if constexpr (!WIDE) gv[i] = gamma_chunk(lane + 64 * i);
 #pragma unroll
     for (int e = 0; e < 8; ++e) gsum[i][e] = 0.f;
   }
@@ -96,14 +102,17 @@ __global__ __launch_bounds__(64 * BWD_WAVES) void rmsnorm_bwd_kernel(int64_t row
     const int64_t row = row_begin + rr;
     if (row >= rows) break;
     const float rs = r[row];
-    u32x4 xv[CH], dv[CH], rv[CH];
+    u32x4 xv[CH], dv[CH], rv[WIDE ? 1 : CH];
+    auto dres_chunk = [&](int c) {
+      return c < chunks && dres ? *(const u32x4*)(dres + row * hidden + c * 8) : u32x4{0u, 0u, 0u, 0u};
+    };
 #pragma unroll
     for (int i = 0; i < CH; ++i) {
       const int c = lane + 64 * i;
       const bool in = c < chunks;
       xv[i] = in ? *(const u32x4*)(x + row * hidden + c * 8) : u32x4{0u, 0u, 0u, 0u};
       dv[i] = in ? *(const u32x4*)(dh + row * hidden + c * 8) : u32x4{0u, 0u, 0u, 0u};
-      rv[i] = in && dres ? *(const u32x4*)(dres + row * hidden + c * 8) : u32x4{0u, 0u, 0u, 0u};
+      if constexpr (!WIDE) rv[i] = dres_chunk(c);
     }
     float dot = 0.f;
 #pragma unroll
@@ -111,7 +120,7 @@ __global__ __launch_bounds__(64 * BWD_WAVES) void rmsnorm_bwd_kernel(int64_t row
       float xf[8], df[8], g[8];
       unpack8(xv[i], xf);
       unpack8(dv[i], df);
-      unpack8(gv[i], g);
+      unpack8(WIDE ? gamma_chunk(lane + 64 * i) : gv[i], g);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         dot += g[e] * df[e] * xf[e];
@@ -127,8 +136,8 @@ __global__ __launch_bounds__(64 * BWD_WAVES) void rmsnorm_bwd_kernel(int64_t row
       float xf[8], df[8], g[8], o[8], rf[8];
       unpack8(xv[i], xf);
       unpack8(dv[i], df);
-      unpack8(gv[i], g);
-      unpack8(rv[i], rf);
+      unpack8(WIDE ? gamma_chunk(c) : gv[i], g);
+      unpack8(WIDE ? dres_chunk(c) : rv[i], rf);
 #pragma unroll
       for (int e = 0; e < 8; ++e) o[e] = rf[e] + rs * g[e] * df[e] - xf[e] * coef;
       *(u32x4*)(dx + row * hidden + c * 8) = pack8(o);
@@ -144,6 +153,82 @@ __global__ __launch_bounds__(64 * BWD_WAVES) void rmsnorm_bwd_kernel(int64_t row
           const int j = (lane + 64 * i) * 8 + e;
           red[j] = w == 0 ? gsum[i][e] : red[j] + gsum[i][e];
         }
+    }
+    __syncthreads();
+  }
+  for (int j = threadIdx.x; j < hidden; j += 64 * BWD_WAVES) partial[(int64_t)blockIdx.x * hidden + j] = red[j];
+}
+
+// The same for rows of more than 8 chunks per lane (hidden > 4096): one row
+// per wave, so that no gain-gradient sums are carried from row to row (with
+// them the kernel above spills): each wave adds its row's dh*x*r into the
+// workgroup's sums in wave order, straight from the row's registers.
+template <int CH>
+__global__ __launch_bounds__(64 * BWD_WAVES) void rmsnorm_bwd_wide_kernel(int64_t rows, int hidden,
+                                                                          const bf16_t* __restrict__ x,
+                                                                          const bf16_t* __restrict__ gamma,
+                                                                          const float* __restrict__ r,
+                                                                          const bf16_t* __restrict__ dh,
+                                                                          const bf16_t* __restrict__ dres,
+                                                                          bf16_t* __restrict__ dx,
+                                                                          float* __restrict__ partial) {
+  __shared__ float red[CH * 512];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int chunks = hidden / 8;
+  const int64_t row = (int64_t)blockIdx.x * BWD_WAVES + wave;
+  const bool valid = row < rows;
+  const float rs = valid ? r[row] : 0.f;
+  u32x4 xv[CH], dv[CH];
+#pragma unroll
+  for (int i = 0; i < CH; ++i) {
+    const int c = lane + 64 * i;
+    const bool in = valid && c < chunks;
+    xv[i] = in ? *(const u32x4*)(x + row * hidden + c * 8) : u32x4{0u, 0u, 0u, 0u};
+    dv[i] = in ? *(const u32x4*)(dh + row * hidden + c * 8) : u32x4{0u, 0u, 0u, 0u};
+  }
+  float dot = 0.f;
+#pragma unroll
+  for (int i = 0; i < CH; ++i) {
+    const int c = lane + 64 * i;
+    float xf[8], df[8], g[8];
+    unpack8(xv[i], xf);
+    unpack8(dv[i], df);
+    unpack8(c < chunks ? *(const u32x4*)(gamma + c * 8) : u32x4{0u, 0u, 0u, 0u}, g);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) dot += g[e] * df[e] * xf[e];
+  }
+  dot = wave_sum(dot);
+  const float coef = rs * rs * rs * dot / (float)hidden;
+  if (valid) {
+#pragma unroll
+    for (int i = 0; i < CH; ++i) {
+      const int c = lane + 64 * i;
+      if (c >= chunks) continue;
+      float xf[8], df[8], g[8], o[8], rf[8];
+      unpack8(xv[i], xf);
+      unpack8(dv[i], df);
+      unpack8(*(const u32x4*)(gamma + c * 8), g);
+      unpack8(dres ? *(const u32x4*)(dres + row * hidden + c * 8) : u32x4{0u, 0u, 0u, 0u}, rf);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] = rf[e] + rs * g[e] * df[e] - xf[e] * coef;
+      *(u32x4*)(dx + row * hidden + c * 8) = pack8(o);
+    }
+  }
+  // the workgroup's column sums, the waves' rows added in wave order (deterministic)
+  for (int w = 0; w < BWD_WAVES; ++w) {
+    if (wave == w) {
+#pragma unroll
+      for (int i = 0; i < CH; ++i) {
+        float xf[8], df[8];
+        unpack8(xv[i], xf);
+        unpack8(dv[i], df);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int j = (lane + 64 * i) * 8 + e;
+          const float v = df[e] * xf[e] * rs;
+          red[j] = w == 0 ? v : red[j] + v;
+        }
+      }
     }
     __syncthreads();
   }
@@ -201,25 +286,37 @@ hipError_t rmsnorm_fwd(int64_t rows, int hidden, float eps, const bf16_t* x, con
   return hipGetLastError();
 }
 
-int rmsnorm_bwd_parts(int64_t rows) { return (int)((rows + BWD_ROWS_PER_BLOCK - 1) / BWD_ROWS_PER_BLOCK); }
+// More than 8 chunks per lane: one row per wave (rmsnorm_bwd_wide_kernel).
+bool rmsnorm_bwd_wide(int hidden) { return (hidden / 8 + 63) / 64 > 8; }
+
+int rmsnorm_bwd_parts(int64_t rows, int hidden) {
+  const int per = rmsnorm_bwd_wide(hidden) ? BWD_WAVES : BWD_ROWS_PER_BLOCK;
+  return (int)((rows + per - 1) / per);
+}
 
 hipError_t rmsnorm_bwd(int64_t rows, int hidden, const bf16_t* x, const bf16_t* gamma, const float* r,
                        const bf16_t* dh, const bf16_t* dres, bf16_t* dx, float* dgamma, int accumulate,
                        float* partial, hipStream_t s) {
   const int ch = (hidden / 8 + 63) / 64;
-  const int parts = rmsnorm_bwd_parts(rows);
+  const int parts = rmsnorm_bwd_parts(rows, hidden);
   const dim3 grid((unsigned)parts), block(64 * BWD_WAVES);
 #define LS_B(CHV)                                                                                       \
   case CHV:                                                                                             \
     hipLaunchKernelGGL((rmsnorm_bwd_kernel<CHV>), grid, block, 0, s, rows, hidden, x, gamma, r, dh, dres, dx, \
                        partial);                                                                        \
     break;
+#define LS_W(CHV)                                                                                            \
+  case CHV:                                                                                                  \
+    hipLaunchKernelGGL((rmsnorm_bwd_wide_kernel<CHV>), grid, block, 0, s, rows, hidden, x, gamma, r, dh, dres, dx, \
+                       partial);                                                                             \
+    break;
   switch (ch) {
     LS_B(1) LS_B(2) LS_B(3) LS_B(4) LS_B(5) LS_B(6) LS_B(7) LS_B(8)
-    LS_B(9) LS_B(10) LS_B(11) LS_B(12) LS_B(13) LS_B(14) LS_B(15) LS_B(16)
+    LS_W(9) LS_W(10) LS_W(11) LS_W(12) LS_W(13) LS_W(14) LS_W(15) LS_W(16)
     default: return hipErrorInvalidValue;
   }
 #undef LS_B
+#undef LS_W
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(column_sum_kernel, dim3((hidden + 63) / 64), dim3(64 * SUM_GROUPS), 0, s, parts, hidden,

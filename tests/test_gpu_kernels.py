@@ -71,7 +71,10 @@ def test_gemm_tn_accumulate(M, N, K, tile):
     assert max_rel(f64(C), 2 * ref) < 1e-5
 
 
-@pytest.mark.parametrize("rows,hidden", [(100, 264), (37, 6656), (1000, 3072), (5, 8)])
+# hidden 3584 and 4096: more than 6 chunks per lane (gamma and dres read where used);
+# 4104, 6656 and 8192: the one-row-per-wave kernel
+@pytest.mark.parametrize("rows,hidden", [(100, 264), (37, 6656), (1000, 3072), (5, 8), (70, 3584), (45, 4096), (50, 4104),
+                                         (20, 8192)])
 def test_rmsnorm(rows, hidden):
     need_gpu()
     say(f"rmsnorm rows={rows} hidden={hidden}")
