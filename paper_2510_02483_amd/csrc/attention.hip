@@ -384,6 +384,31 @@ template <int D>
 LS_DEV void unrotate_store(const f32x16 (&acc)[D / 32], float scale, const float* rope_cs, int seq, int pos, int lh,
                            bf16_t* row) {
   constexpr int HALF = D / 2, IP = HALF / 32;
+  if (rope_cs == nullptr) {
+#pragma unroll
+    for (int i = 0; i < D / 32; ++i)
+#pragma unroll
+      for (int rq = 0; rq < 4; ++rq) {
+        const int d = 32 * i + 8 * rq + 4 * lh;
+        *(u32x2*)(row + d) = u32x2{pack_bf2(acc[i][4 * rq] * scale, acc[i][4 * rq + 1] * scale),
+                                   pack_bf2(acc[i][4 * rq + 2] * scale, acc[i][4 * rq + 3] * scale)};
+      }
+    return;
+  }
+  // cos and sin of the lane's angle indices (4 consecutive ones per 8-column
+  // group, 16-byte loads), all in flight before the rotations use them; the
+  // second half of the head uses the angles of the first
+  const float* cb = rope_cs + (int64_t)pos * HALF;
+  const float* sb = rope_cs + (int64_t)seq * HALF + (int64_t)pos * HALF;
+  f32x4 c4[IP][4], s4[IP][4];
+#pragma unroll
+  for (int i = 0; i < IP; ++i)
+#pragma unroll
+    for (int rq = 0; rq < 4; ++rq) {
+      const int d = 32 * i + 8 * rq + 4 * lh;
+      c4[i][rq] = *(const f32x4*)(cb + d);
+      s4[i][rq] = *(const f32x4*)(sb + d);
+    }
 #pragma unroll
   for (int i = 0; i < D / 32; ++i)
 #pragma unroll
@@ -393,19 +418,12 @@ LS_DEV void unrotate_store(const f32x16 (&acc)[D / 32], float scale, const float
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const float x = acc[i][4 * rq + e] * scale;
-        if (rope_cs == nullptr) {
-          out[e] = x;
-        } else if (i < IP) {  // first half: x1' = x1 cos + x2 sin
+        if (i < IP) {  // first half: x1' = x1 cos + x2 sin
           const float x2 = acc[i + IP][4 * rq + e] * scale;
-          const float c = rope_cs[(int64_t)pos * HALF + d + e];
-          const float sn = rope_cs[(int64_t)seq * HALF + (int64_t)pos * HALF + d + e];
-          out[e] = x * c + x2 * sn;
+          out[e] = x * c4[i][rq][e] + x2 * s4[i][rq][e];
         } else {  // second half: x2' = x2 cos - x1 sin
           const float x1 = acc[i - IP][4 * rq + e] * scale;
-          const int dl = d - HALF + e;
-          const float c = rope_cs[(int64_t)pos * HALF + dl];
-          const float sn = rope_cs[(int64_t)seq * HALF + (int64_t)pos * HALF + dl];
-          out[e] = x * c - x1 * sn;
+          out[e] = x * c4[i - IP][rq][e] - x1 * s4[i - IP][rq][e];
         }
       }
       *(u32x2*)(row + d) = u32x2{pack_bf2(out[0], out[1]), pack_bf2(out[2], out[3])};
